@@ -1,0 +1,264 @@
+/*
+ * CPU oracle for multi-stage KV-cache live migration (Llumnix, arXiv
+ * 2406.03243).
+ *
+ * TEST INFRASTRUCTURE ONLY.  Nothing in the product path may link, load or
+ * call this file; only the test suite, the smoke check and the CPU-baseline
+ * leg of the benchmark do.  It shares no code, header, constant or helper
+ * with the GPU library: it is a plain, slow, obviously correct restatement
+ * of what a migration computes, written against host copies of the pools.
+ *
+ * What a migration is (Llumnix §4.2, "Live Migration of LLM Requests"): the
+ * KV cache of a running request is append-only, so the blocks it already
+ * filled can be copied from the source instance's block pool to blocks the
+ * destination reserved, stage after stage, while decoding continues; the
+ * last stage copies what the final iteration added.  A migration therefore
+ * reaches exactly a byte copy of whole KV blocks, and this oracle is that
+ * definition written out.
+ *
+ * Pool layout (vLLM's paged KV cache, Llumnix §2 "Batching and memory
+ * management" and §5 "Block fusion"): for every layer l there is one K
+ * tensor and one V tensor of shape [num_blocks, block_size, kv_heads,
+ * head_dim].  One (layer, K or V, block) tile is tile_bytes = block_size *
+ * kv_heads * head_dim * elem_bytes contiguous bytes; token slot s of a block
+ * occupies slot_bytes = kv_heads * head_dim * elem_bytes bytes at offset
+ * s * slot_bytes inside its tile.
+ *
+ * Every routine below moves bytes with memcpy/memcmp and never interprets
+ * them as numbers, so NaN payloads, signed zeros and subnormals pass through
+ * untouched.
+ *
+ * Error classes (the same classes the library reports, defined here on
+ * their own): ORACLE_OK, ORACLE_EINVAL (bad range or argument, duplicate
+ * ids), ORACLE_ENOSPC (the destination could not reserve the blocks the
+ * stage needs: the failed pre-allocation of the handshake, Llumnix §4.2),
+ * ORACLE_ERANGE (a negative block id).
+ */
+#include <stdint.h>
+#include <string.h>
+
+#define ORACLE_OK 0
+#define ORACLE_EINVAL (-1)
+#define ORACLE_ENOSPC (-2)
+#define ORACLE_ERANGE (-3)
+
+/*
+ * Plan one migration stage (Llumnix §4.2: before each stage the source asks
+ * the destination to pre-allocate "the number of blocks to migrate"; stage k
+ * copies the KV produced since stage k-1).
+ *
+ * The stage covers tokens [from_tok, to_tok) of a request whose first `len`
+ * tokens are resident in the source pool.  Logical block j holds tokens
+ * [j*bs, (j+1)*bs).  The stage's logical blocks are found by walking the
+ * tokens one at a time and recording each block the walk enters; logical
+ * block J[k] is paired with the k-th entry of the destination free list
+ * (first come, first served).
+ *
+ * Readings of the paper that this follows:
+ *  - a non-final stage copies only whole blocks, so from_tok must sit on a
+ *    block boundary, and to_tok must too unless it is the end of the
+ *    sequence (the last, partial block is copied by the final stage only);
+ *  - the mapping takes destination blocks from the head of the free list in
+ *    ascending logical order; the caller advances its free list by *out_n.
+ *
+ * Checks, in this order (the first failing one decides the result):
+ *   1. out_n present                                 (else ORACLE_EINVAL);
+ *   2. bs >= 1, 0 <= from_tok <= to_tok <= len;
+ *   3. from_tok on a block boundary; to_tok on one unless to_tok == len;
+ *   4. no negative table, free-list or output length;
+ *   5. the source table holds every block of the first len tokens (and is
+ *      present when it must hold any);
+ *   6. the free list holds enough blocks            (else ORACLE_ENOSPC);
+ *   7. the outputs hold the stage, and the free list and outputs are
+ *      present when the stage is not empty;
+ *   8. no negative block id among the stage's pairs  (else ORACLE_ERANGE);
+ *   9. no block id repeated among the stage's sources, nor among its
+ *      destinations.
+ * Checks 2-5, 7 and 9 fail with ORACLE_EINVAL.
+ * On any error *out_n is 0 (when out_n exists) and nothing else is written.
+ */
+int oracle_plan(const int32_t *src_table, int64_t src_table_len,
+                const int32_t *dst_free_list, int64_t dst_free_len,
+                int64_t len, int64_t from_tok, int64_t to_tok, int32_t bs,
+                int32_t *out_src, int32_t *out_dst, int64_t out_cap,
+                int64_t *out_n)
+{
+    if (out_n == NULL)
+        return ORACLE_EINVAL;
+    *out_n = 0;
+    if (bs < 1 || len < 0 || from_tok < 0 || from_tok > to_tok || to_tok > len)
+        return ORACLE_EINVAL;
+    if (from_tok % bs != 0)
+        return ORACLE_EINVAL;
+    if (to_tok % bs != 0 && to_tok != len)
+        return ORACLE_EINVAL;
+    if (src_table_len < 0 || dst_free_len < 0 || out_cap < 0)
+        return ORACLE_EINVAL;
+
+    /* Blocks that hold the first len tokens: walk every token. */
+    int64_t blocks_of_len = 0;
+    int64_t last = -1;
+    for (int64_t t = 0; t < len; t++) {
+        if (t / bs != last) {
+            last = t / bs;
+            blocks_of_len++;
+        }
+    }
+    if (src_table_len < blocks_of_len)
+        return ORACLE_EINVAL;
+    if (blocks_of_len > 0 && src_table == NULL)
+        return ORACLE_EINVAL;
+
+    /* Blocks the stage touches: walk the stage's tokens. */
+    int64_t n = 0;
+    int64_t first_block = -1;
+    last = -1;
+    for (int64_t t = from_tok; t < to_tok; t++) {
+        if (t / bs != last) {
+            last = t / bs;
+            if (first_block < 0)
+                first_block = last;
+            n++;
+        }
+    }
+    if (n > dst_free_len)
+        return ORACLE_ENOSPC;
+    if (n > out_cap)
+        return ORACLE_EINVAL;
+    if (n > 0 && (dst_free_list == NULL || out_src == NULL || out_dst == NULL))
+        return ORACLE_EINVAL;
+
+    for (int64_t k = 0; k < n; k++) {
+        if (src_table[first_block + k] < 0 || dst_free_list[k] < 0)
+            return ORACLE_ERANGE;
+    }
+    /* Pairwise comparison: slow, but plainly right. */
+    for (int64_t a = 0; a < n; a++) {
+        for (int64_t b = a + 1; b < n; b++) {
+            if (src_table[first_block + a] == src_table[first_block + b])
+                return ORACLE_EINVAL;
+            if (dst_free_list[a] == dst_free_list[b])
+                return ORACLE_EINVAL;
+        }
+    }
+
+    for (int64_t k = 0; k < n; k++) {
+        out_src[k] = src_table[first_block + k];
+        out_dst[k] = dst_free_list[k];
+    }
+    *out_n = n;
+    return ORACLE_OK;
+}
+
+/*
+ * Copy one stage (Llumnix §4.2): for every pair (s, d), every layer l and
+ * both K and V, the destination tile d receives the bytes of source tile s.
+ * src_k[l], src_v[l], dst_k[l], dst_v[l] are host copies of the layer
+ * tensors; tile_bytes is the size of one (layer, K/V, block) tile.
+ */
+void oracle_copy(uint8_t *const *src_k, uint8_t *const *src_v,
+                 uint8_t *const *dst_k, uint8_t *const *dst_v,
+                 int32_t num_layers, int64_t tile_bytes,
+                 const int32_t *map_src, const int32_t *map_dst, int64_t n)
+{
+    for (int64_t i = 0; i < n; i++) {
+        for (int32_t l = 0; l < num_layers; l++) {
+            memcpy(dst_k[l] + (int64_t)map_dst[i] * tile_bytes,
+                   src_k[l] + (int64_t)map_src[i] * tile_bytes, (size_t)tile_bytes);
+            memcpy(dst_v[l] + (int64_t)map_dst[i] * tile_bytes,
+                   src_v[l] + (int64_t)map_src[i] * tile_bytes, (size_t)tile_bytes);
+        }
+    }
+}
+
+/*
+ * Block fusion, sending side (Llumnix §5 "Block fusion": the scattered
+ * per-layer K/V blocks of a request are gathered into one contiguous buffer
+ * so they travel as a single message).  The buffer is laid out
+ * [layer][K=0, V=1][i][tile_bytes], i in the order of blocks[].
+ */
+void oracle_pack(uint8_t *const *pool_k, uint8_t *const *pool_v,
+                 int32_t num_layers, int64_t tile_bytes,
+                 const int32_t *blocks, int64_t n, uint8_t *staging)
+{
+    for (int32_t l = 0; l < num_layers; l++) {
+        for (int kv = 0; kv < 2; kv++) {
+            uint8_t *const *pool = (kv == 0) ? pool_k : pool_v;
+            for (int64_t i = 0; i < n; i++) {
+                int64_t slot = ((int64_t)l * 2 + kv) * n + i;
+                memcpy(staging + slot * tile_bytes,
+                       pool[l] + (int64_t)blocks[i] * tile_bytes, (size_t)tile_bytes);
+            }
+        }
+    }
+}
+
+/* Block fusion, receiving side: the inverse of oracle_pack. */
+void oracle_unpack(uint8_t *const *pool_k, uint8_t *const *pool_v,
+                   int32_t num_layers, int64_t tile_bytes,
+                   const int32_t *blocks, int64_t n, const uint8_t *staging)
+{
+    for (int32_t l = 0; l < num_layers; l++) {
+        for (int kv = 0; kv < 2; kv++) {
+            uint8_t *const *pool = (kv == 0) ? pool_k : pool_v;
+            for (int64_t i = 0; i < n; i++) {
+                int64_t slot = ((int64_t)l * 2 + kv) * n + i;
+                memcpy(pool[l] + (int64_t)blocks[i] * tile_bytes,
+                       staging + slot * tile_bytes, (size_t)tile_bytes);
+            }
+        }
+    }
+}
+
+/*
+ * Decoding appends KV (Llumnix §4.2: each iteration appends the KV of its
+ * token and leaves earlier KV unchanged).  Writes tokens
+ * [from_tok, from_tok + n_tok) into the pool through the request's block
+ * table; data is laid out [layer][K=0, V=1][token][slot_bytes].
+ */
+void oracle_write_tokens(uint8_t *const *pool_k, uint8_t *const *pool_v,
+                         int32_t num_layers, int32_t bs, int64_t slot_bytes,
+                         const int32_t *table, int64_t from_tok, int64_t n_tok,
+                         const uint8_t *data)
+{
+    int64_t tile_bytes = (int64_t)bs * slot_bytes;
+    for (int32_t l = 0; l < num_layers; l++) {
+        for (int kv = 0; kv < 2; kv++) {
+            uint8_t *const *pool = (kv == 0) ? pool_k : pool_v;
+            for (int64_t j = 0; j < n_tok; j++) {
+                int64_t t = from_tok + j;
+                uint8_t *slot = pool[l] + (int64_t)table[t / bs] * tile_bytes
+                              + (t % bs) * slot_bytes;
+                memcpy(slot, data + (((int64_t)l * 2 + kv) * n_tok + j) * slot_bytes,
+                       (size_t)slot_bytes);
+            }
+        }
+    }
+}
+
+/*
+ * Token identity, the property a migration must establish: for every token
+ * t < len, every layer and both K and V, the bytes of t's slot reached
+ * through table_a in pool a equal those reached through table_b in pool b.
+ * Returns -1 when all match, else the first token that differs.
+ */
+int64_t oracle_first_token_mismatch(uint8_t *const *a_k, uint8_t *const *a_v,
+                                    const int32_t *table_a,
+                                    uint8_t *const *b_k, uint8_t *const *b_v,
+                                    const int32_t *table_b,
+                                    int32_t num_layers, int32_t bs,
+                                    int64_t slot_bytes, int64_t len)
+{
+    int64_t tile_bytes = (int64_t)bs * slot_bytes;
+    for (int64_t t = 0; t < len; t++) {
+        for (int32_t l = 0; l < num_layers; l++) {
+            int64_t off_a = (int64_t)table_a[t / bs] * tile_bytes + (t % bs) * slot_bytes;
+            int64_t off_b = (int64_t)table_b[t / bs] * tile_bytes + (t % bs) * slot_bytes;
+            if (memcmp(a_k[l] + off_a, b_k[l] + off_b, (size_t)slot_bytes) != 0)
+                return t;
+            if (memcmp(a_v[l] + off_a, b_v[l] + off_b, (size_t)slot_bytes) != 0)
+                return t;
+        }
+    }
+    return -1;
+}

@@ -1,0 +1,90 @@
+"""Every plausible single mistake planted in a copy of the CPU oracle must
+fail at least one pin: evidence that the pins can tell a wrong oracle from a
+right one.  The mistakes are planted in temporary copies of the oracle's C
+source; the oracle itself is never changed."""
+import json
+import os
+import subprocess
+import sys
+import tempfile
+
+import oracle
+
+# (name, text in the oracle's source, replacement, which occurrence)
+MUTANTS = [
+    ("plan_dst_reversed", "out_dst[k] = dst_free_list[k];", "out_dst[k] = dst_free_list[n - 1 - k];", 0),
+    ("plan_src_no_offset", "out_src[k] = src_table[first_block + k];", "out_src[k] = src_table[k];", 0),
+    ("plan_walk_inclusive", "for (int64_t t = from_tok; t < to_tok; t++) {",
+     "for (int64_t t = from_tok; t <= to_tok; t++) {", 0),
+    ("plan_enospc_off_by_one", "if (n > dst_free_len)", "if (n >= dst_free_len)", 0),
+    ("plan_rejects_final_partial", "if (to_tok % bs != 0 && to_tok != len)", "if (to_tok % bs != 0)", 0),
+    ("plan_no_boundary_check", "if (from_tok % bs != 0)", "if (0)", 0),
+    ("plan_no_dst_duplicate_check", "if (dst_free_list[a] == dst_free_list[b])", "if (0)", 0),
+    ("plan_no_src_duplicate_check", "if (src_table[first_block + a] == src_table[first_block + b])",
+     "if (0)", 0),
+    ("plan_erange_missed", "if (src_table[first_block + k] < 0 || dst_free_list[k] < 0)",
+     "if (src_table[first_block + k] < -1 || dst_free_list[k] < -5)", 0),
+    ("plan_short_table_accepted", "if (src_table_len < blocks_of_len)",
+     "if (src_table_len < blocks_of_len - 1)", 0),
+    ("plan_out_cap_unchecked", "if (n > out_cap)", "if (n > out_cap + 1)", 0),
+    ("copy_pairs_misaligned", "src_k[l] + (int64_t)map_src[i] * tile_bytes",
+     "src_k[l] + (int64_t)map_src[n - 1 - i] * tile_bytes", 0),
+    ("copy_v_from_k", "src_v[l] + (int64_t)map_src[i] * tile_bytes",
+     "src_k[l] + (int64_t)map_src[i] * tile_bytes", 0),
+    ("copy_drops_last_layer", "for (int32_t l = 0; l < num_layers; l++) {\n            memcpy(dst_k[l]",
+     "for (int32_t l = 0; l < num_layers - 1; l++) {\n            memcpy(dst_k[l]", 0),
+    ("pack_transposed", "int64_t slot = ((int64_t)l * 2 + kv) * n + i;",
+     "int64_t slot = (i * 2 + kv) * num_layers + l;", 0),
+    ("unpack_reversed", "memcpy(pool[l] + (int64_t)blocks[i] * tile_bytes,",
+     "memcpy(pool[l] + (int64_t)blocks[n - 1 - i] * tile_bytes,", 0),
+    ("write_tokens_slot_shift", "+ (t % bs) * slot_bytes;", "+ ((t + 1) % bs) * slot_bytes;", 0),
+    ("write_tokens_kv_swapped", "uint8_t *const *pool = (kv == 0) ? pool_k : pool_v;",
+     "uint8_t *const *pool = (kv == 0) ? pool_v : pool_k;", 2),
+    ("mismatch_skips_v", "if (memcmp(a_v[l] + off_a, b_v[l] + off_b, (size_t)slot_bytes) != 0)",
+     "if (0)", 0),
+    ("mismatch_skips_last_token", "for (int64_t t = 0; t < len; t++) {\n        for (int32_t l = 0;",
+     "for (int64_t t = 0; t < len - 1; t++) {\n        for (int32_t l = 0;", 0),
+]
+
+RUNNER = r"""
+import json, sys
+sys.path[:0] = [sys.argv[1], sys.argv[2]]
+import pins
+from oracle import Oracle
+out = {}
+for name, lib in json.loads(sys.argv[3]).items():
+    orc = Oracle(lib)
+    failed = []
+    for pin in pins.ALL_PINS:
+        try:
+            pin(orc)
+        except Exception:            # a wrong result, or an error where none is due
+            failed.append(pin.__name__)
+    out[name] = failed
+print(json.dumps(out))
+"""
+
+
+def _mutate(src, old, new, which):
+    parts = src.split(old)
+    assert len(parts) > which + 1, f"mutation site not found: {old!r}"
+    return old.join(parts[:which + 1]) + new + old.join(parts[which + 1:])
+
+
+def test_every_planted_mistake_fails_a_pin():
+    src = open(oracle.SOURCE).read()
+    tests_dir = os.path.dirname(os.path.abspath(__file__))
+    root = os.path.dirname(tests_dir)
+    with tempfile.TemporaryDirectory() as tmp:
+        libs = {}
+        for name, old, new, which in MUTANTS:
+            path = os.path.join(tmp, name + ".c")
+            with open(path, "w") as f:
+                f.write(_mutate(src, old, new, which))
+            libs[name] = oracle.build(path, os.path.join(tmp, name + ".so"), quiet=True)
+        res = subprocess.run([sys.executable, "-c", RUNNER, root, tests_dir, json.dumps(libs)],
+                             capture_output=True, text=True, timeout=600)
+        assert res.returncode == 0, res.stderr[-3000:]
+        caught = json.loads(res.stdout.strip().splitlines()[-1])
+    missed = [name for name, failed in caught.items() if not failed]
+    assert not missed, f"mutants no pin catches: {missed}"
