@@ -1,0 +1,178 @@
+/*
+ * llmig: multi-stage live migration of a request's paged KV cache between two
+ * block pools on one AMD Instinct MI355X (gfx950).
+ *
+ * What it implements (Llumnix, arXiv 2406.03243, §4.2 "Live Migration of LLM
+ * Requests"): the KV cache of a decoding request only ever grows at its end,
+ * so the blocks it has already filled can be copied to the destination
+ * instance while decoding goes on.  Stage 0 copies every filled block; each
+ * later stage copies the blocks filled during the previous one; the final
+ * stage, run after the request has been drained from its batch, copies what
+ * is left.  Only that last stage is downtime.  Before every stage the
+ * destination reserves the blocks the stage needs (the handshake's
+ * pre-allocation, §4.2).  §5 "Block fusion" gathers a request's scattered
+ * per-layer K/V blocks into one contiguous buffer so they move as one
+ * message; llmig_pack / llmig_unpack are that gather and its inverse, and
+ * llmig_stage copies pool to pool directly, since both pools sit on one GPU.
+ *
+ * Pool layout (vLLM paged KV cache, §2 "Batching and memory management"):
+ * every layer l has a K tensor and a V tensor of shape
+ * [num_blocks, block_size, num_kv_heads, head_dim], each element elem_bytes
+ * wide.  One (layer, K or V, block) tile is
+ *     tile_bytes = block_size * num_kv_heads * head_dim * elem_bytes
+ * contiguous bytes (128 KB for 16 tokens of 16-bit LLaMA-7B, §5).  The copy
+ * moves whole tiles as raw bytes and never converts them, so any 16-bit
+ * format (fp16, bf16) and any bit pattern (NaN payloads, -0, subnormals)
+ * arrives unchanged.
+ *
+ * Error convention: every entry point returns LLMIG_OK (0) or a negative
+ * code.  All argument checks run before anything is enqueued, so a call that
+ * fails has no effect.  Nothing throws or aborts across this interface.
+ *
+ * Threads and streams: llmig_plan is pure.  The other calls only enqueue on
+ * the stream they are given and may be called from several threads on
+ * distinct streams; a pool handle is immutable after creation and may be
+ * shared.  Ordering against the writes of decoding is the caller's job
+ * (events between the decode stream and the migration stream), and a
+ * non-final stage must only contain blocks that decoding will not write
+ * again (the full blocks), which llmig_plan enforces.
+ */
+#ifndef LLMIG_H
+#define LLMIG_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define LLMIG_OK 0
+#define LLMIG_EINVAL (-1) /* bad argument, range, alignment, shape or duplicate id */
+#define LLMIG_ENOSPC (-2) /* the destination free list cannot hold the stage (§4.2: the
+                             pre-allocation fails and the migration aborts) */
+#define LLMIG_ERANGE (-3) /* a block id outside [0, num_blocks) */
+#define LLMIG_EHIP (-4)   /* the HIP runtime reported an error: see llmig_last_hip_error */
+
+/* Describes a caller-owned pool.  k_ptrs and v_ptrs are HOST arrays of
+ * num_layers DEVICE addresses, one per layer tensor
+ * [num_blocks, block_size, num_kv_heads, head_dim]; each address must be
+ * 16-byte aligned and tile_bytes a multiple of 16.  The arrays are read
+ * during llmig_pool_create only. */
+typedef struct llmig_pool_desc {
+    int32_t num_layers;
+    int32_t num_blocks;
+    int32_t block_size;
+    int32_t num_kv_heads;
+    int32_t head_dim;
+    int32_t elem_bytes;
+    const uint64_t *k_ptrs;
+    const uint64_t *v_ptrs;
+} llmig_pool_desc;
+
+typedef struct llmig_pool llmig_pool;
+
+/* Registers a pool on the current HIP device: validates the description and
+ * copies the per-layer address table to device memory once.  The library
+ * owns only that table; the pool memory stays the caller's and must outlive
+ * the handle.  Errors: LLMIG_EINVAL (a non-positive size, a null array or
+ * address, misalignment, a tile over 2^31 bytes), LLMIG_EHIP. */
+int llmig_pool_create(const llmig_pool_desc *desc, llmig_pool **out);
+
+/* Frees the handle and its device table (not the pool memory).  The caller
+ * must make sure no enqueued work still uses the handle.  NULL is allowed. */
+void llmig_pool_destroy(llmig_pool *pool);
+
+/* Bytes of one (layer, K/V, block) tile of the pool, or -1 for NULL. */
+int64_t llmig_pool_tile_bytes(const llmig_pool *pool);
+
+/* Plans one migration stage (§4.2: before each stage the destination
+ * pre-allocates the blocks the stage migrates).  Pure host function: no GPU
+ * call, no allocation, reentrant.
+ *
+ * The request has `len` tokens resident in the source pool; logical block j
+ * holds tokens [j*block_size, (j+1)*block_size) and lives in source block
+ * src_table[j].  The stage covers tokens [from_tok, to_tok): its logical
+ * blocks are from_tok/block_size .. ceil(to_tok/block_size)-1, and the k-th
+ * of them is paired with dst_free_list[k] (destination blocks are taken from
+ * the head of the free list, in ascending logical order).  On success
+ * out_src[k], out_dst[k] for k < *out_n hold the pairs; *out_n is also the
+ * number of free-list entries consumed, which the caller drops from the
+ * head of its free list.
+ *
+ * A non-final stage copies only whole blocks: from_tok must be a multiple of
+ * block_size, and so must to_tok unless to_tok == len (the final stage,
+ * which also takes the partially filled last block).
+ *
+ * Checks, in order (the first failure decides): out_n non-NULL; block_size
+ * >= 1 and 0 <= from_tok <= to_tok <= len; the block-boundary rule above;
+ * no negative length or capacity; src_table_len >= ceil(len/block_size)
+ * (and src_table non-NULL if that is positive) -- all LLMIG_EINVAL; the
+ * free list holds the stage -- else LLMIG_ENOSPC; out_cap holds the stage
+ * and the arrays are non-NULL when the stage is not empty -- LLMIG_EINVAL;
+ * no negative id among the stage's pairs -- LLMIG_ERANGE; no id repeated
+ * among the stage's sources nor among its destinations -- LLMIG_EINVAL.
+ * On error *out_n = 0 (if out_n is non-NULL) and nothing else is written. */
+int llmig_plan(const int32_t *src_table, int64_t src_table_len,
+               const int32_t *dst_free_list, int64_t dst_free_len,
+               int64_t len, int64_t from_tok, int64_t to_tok, int32_t block_size,
+               int32_t *out_src, int32_t *out_dst, int64_t out_cap, int64_t *out_n);
+
+/* Copies one stage pool to pool (§4.2): for every i < n, every layer and
+ * both K and V, tile map_dst[i] of dst receives the bytes of tile map_src[i]
+ * of src.  Enqueue only: returns once the work is launched on `stream` (a
+ * hipStream_t; NULL is the null stream).
+ *
+ * map_on_device = 0: map_src/map_dst are host arrays, which may be reused as
+ * soon as the call returns (the ids travel inside the kernel arguments); ids
+ * are range-checked (LLMIG_ERANGE) and repeated destination ids rejected
+ * (LLMIG_EINVAL).  map_on_device = 1: device arrays of int32 that must stay
+ * valid until the work completes; the caller guarantees the ids are in range
+ * and that no destination id repeats.
+ *
+ * src and dst must be different pools whose layer, block_size, head and
+ * element sizes match (num_blocks may differ) and whose memory does not
+ * overlap; else LLMIG_EINVAL.  n = 0 does nothing.  A batched migration of
+ * several requests concatenates their pairs into one call. */
+int llmig_stage(const llmig_pool *src, const llmig_pool *dst,
+                const int32_t *map_src, const int32_t *map_dst, int64_t n,
+                int map_on_device, void *stream);
+
+/* Block fusion, sending side (§5 "Block fusion"): gathers tiles of the
+ * listed source blocks into the contiguous buffer `staging`, laid out
+ * [num_layers][K=0, V=1][n][tile_bytes] with i in the order of blocks[].
+ * staging is device memory or pinned host memory mapped for the device
+ * (hipHostMalloc); it is caller-owned, 16-byte aligned, and staging_bytes
+ * must be at least n * num_layers * 2 * tile_bytes (else LLMIG_EINVAL).
+ * blocks / map_on_device as for llmig_stage (ids checked against the pool
+ * when on the host; repeats are allowed). */
+int llmig_pack(const llmig_pool *src, const int32_t *blocks, int64_t n, int map_on_device,
+               void *staging, int64_t staging_bytes, void *stream);
+
+/* Block fusion, receiving side: scatters a buffer laid out as llmig_pack
+ * writes it into the listed destination blocks.  Repeated ids are rejected
+ * (LLMIG_EINVAL) when the list is on the host. */
+int llmig_unpack(const llmig_pool *dst, const int32_t *blocks, int64_t n, int map_on_device,
+                 const void *staging, int64_t staging_bytes, void *stream);
+
+/* Stand-in for decoding's KV write (§4.2: every iteration appends its
+ * token's K and V and leaves earlier ones unchanged): writes tokens
+ * [from_tok, from_tok + n_tok) of a request into `pool` through its host
+ * block table.  data is device memory laid out
+ * [num_layers][K=0, V=1][n_tok][num_kv_heads * head_dim * elem_bytes].
+ * table_len must cover the last token (LLMIG_EINVAL), ids are
+ * range-checked (LLMIG_ERANGE).  Used to drive multi-stage migrations
+ * without a model. */
+int llmig_write_tokens(const llmig_pool *pool, const int32_t *table, int64_t table_len,
+                       int64_t from_tok, int64_t n_tok, const void *data, void *stream);
+
+/* Static description of a code; never NULL. */
+const char *llmig_strerror(int code);
+
+/* The hipError_t behind the calling thread's last LLMIG_EHIP (0 if none). */
+int llmig_last_hip_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* LLMIG_H */

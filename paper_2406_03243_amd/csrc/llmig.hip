@@ -1,0 +1,659 @@
+// llmig: multi-stage KV-cache live migration on MI355X (gfx950).
+//
+// Kernels and C-ABI host code behind include/llmig.h.  The method is the
+// live migration of Llumnix (arXiv 2406.03243) §4.2 with the block fusion
+// of §5; the interface comments in llmig.h state what every call computes.
+//
+// Kernel design (CDNA4, wave64):
+//  * The work of a call is a list of tiles, one per (pair, layer, K/V); a
+//    tile is tile_bytes contiguous bytes on both sides.  A tile is cut into
+//    rows of 4 KiB (256 lanes x 16 B), and a workgroup item is a chunk of up
+//    to ROWS rows of one tile: each lane issues all of its 16-byte loads
+//    (global_load_dwordx4) before its first store, so every lane keeps
+//    ROWS x 16 B in flight and each wavefront instruction moves 1 KiB of
+//    contiguous, fully coalesced memory.  Bulk copies use 8-row chunks;
+//    small copies (a final stage) use 2-row chunks to spread over more CUs.
+//  * The block ids of an item are wavefront-uniform; they and the per-layer
+//    base addresses are read with scalar loads, so the only vector memory
+//    traffic is the copy itself.
+//  * A stage's (src, dst) ids travel inside the kernel arguments (up to
+//    kInlinePairs per launch), so a stage needs no mapping upload and no
+//    device allocation: the short final stage costs one launch.
+//  * No LDS: both sides have the same byte layout inside a tile, so data
+//    goes straight from the load registers to the store.  No MFMA: a copy
+//    has no arithmetic.
+//  * Stores are non-temporal: migrated KV is not read again by this GPU
+//    soon, and streaming it past the caches leaves them to the decode work
+//    running beside the migration.
+
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cstdint>
+#include <cstring>
+#include <new>
+#include <utility>
+#include <vector>
+
+#include "llmig.h"
+
+struct llmig_pool {
+    int32_t num_layers, num_blocks, block_size, num_kv_heads, head_dim, elem_bytes;
+    int64_t tile_bytes;
+    int device;
+    uint64_t *d_tab;                                  // device [2 * L]: K bases, then V bases
+    std::vector<std::pair<uint64_t, uint64_t>> spans; // sorted [begin, end) of every layer tensor
+};
+
+namespace {
+
+constexpr int kThreads = 256;                 // 4 wavefronts of 64 lanes
+constexpr uint32_t kRowBytes = kThreads * 16; // one 16-byte word per lane
+constexpr int kBulkRows = 8;                  // rows per item of a bulk copy: 32 KiB in flight
+constexpr int kSmallRows = 2;                 // rows per item of a small (latency-bound) copy
+constexpr uint32_t kBulkItemsPerCU = 16;      // a launch with fewer items than this per CU is small
+constexpr int kInlinePairs = 256;             // ids carried in the kernel arguments per launch
+
+typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+
+thread_local int g_last_hip_error = 0;
+
+int hip_error(hipError_t e)
+{
+    g_last_hip_error = static_cast<int>(e);
+    return LLMIG_EHIP;
+}
+
+enum Side { kPool = 0, kLinear = 1 };
+
+// Arguments of one copy launch.  Pool sides address tile (l, kv, id) at
+// tab[kv * L + l] + id * tile_bytes; linear sides address pair i of plane
+// (l, kv) at lin + ((l * 2 + kv) * lin_pairs + lin_first + i) * tile_bytes.
+struct CopyArgs {
+    const uint64_t *src_tab;
+    const uint64_t *dst_tab;
+    const uint8_t *src_lin;
+    uint8_t *dst_lin;
+    const int32_t *src_ids_dev; // device id lists (null when the ids are inline)
+    const int32_t *dst_ids_dev;
+    uint32_t tile_bytes;
+    uint32_t num_layers;
+    uint32_t pairs;             // pairs in this launch
+    uint32_t chunks_per_tile;
+    uint32_t rows_per_chunk;    // <= ROWS of the kernel
+    uint32_t items;             // pairs * 2 * num_layers * chunks_per_tile
+    uint32_t lin_first;         // this launch's first pair within the whole call
+    uint32_t lin_pairs;         // pairs in the whole call
+    int32_t src_ids[kInlinePairs];
+    int32_t dst_ids[kInlinePairs];
+};
+
+// Address spaces: global for the copied bytes (global_load/global_store
+// instead of flat), constant for the small read-only tables so uniform
+// reads of them become scalar loads.
+#define LLMIG_GLOBAL __attribute__((address_space(1)))
+#define LLMIG_CONSTANT __attribute__((address_space(4)))
+
+__device__ __forceinline__ uint32_t uniform(uint32_t x)
+{
+    return __builtin_amdgcn_readfirstlane(x);
+}
+
+__device__ __forceinline__ uint64_t table_entry(const uint64_t *tab, uint32_t k)
+{
+    return ((const LLMIG_CONSTANT uint64_t *)tab)[k]; // address-space cast
+}
+
+__device__ __forceinline__ int32_t id_entry(const int32_t *ids, uint32_t k)
+{
+    return ((const LLMIG_CONSTANT int32_t *)ids)[k];
+}
+
+__device__ __forceinline__ u32x4 load16(const uint8_t *p)
+{
+    return *(const LLMIG_GLOBAL u32x4 *)p;
+}
+
+__device__ __forceinline__ void store16(uint8_t *p, u32x4 v)
+{
+    __builtin_nontemporal_store(v, (LLMIG_GLOBAL u32x4 *)p);
+}
+
+template <int SRC, int DST, bool INLINE_IDS, int ROWS>
+__global__ void __launch_bounds__(kThreads) copy_tiles(const CopyArgs a)
+{
+    const uint32_t lane_off = threadIdx.x * 16u;
+    const uint32_t full_rows = a.tile_bytes / kRowBytes; // complete 4 KiB rows of a tile
+    for (uint32_t item = blockIdx.x; item < a.items; item += gridDim.x) {
+        const uint32_t tile = item / a.chunks_per_tile;
+        const uint32_t chunk = item - tile * a.chunks_per_tile;
+        const uint32_t plane = tile / a.pairs; // layer * 2 + kv
+        const uint32_t i = tile - plane * a.pairs;
+        const uint32_t layer = plane >> 1, kv = plane & 1u;
+
+        const uint8_t *s;
+        uint8_t *d;
+        if (SRC == kPool) {
+            const int32_t id = INLINE_IDS ? a.src_ids[i] : id_entry(a.src_ids_dev, i);
+            s = reinterpret_cast<const uint8_t *>(table_entry(a.src_tab, kv * a.num_layers + layer)) +
+                static_cast<uint64_t>(uniform(static_cast<uint32_t>(id))) * a.tile_bytes;
+        } else {
+            s = a.src_lin + (static_cast<uint64_t>(plane) * a.lin_pairs + a.lin_first + i) * a.tile_bytes;
+        }
+        if (DST == kPool) {
+            const int32_t id = INLINE_IDS ? a.dst_ids[i] : id_entry(a.dst_ids_dev, i);
+            d = reinterpret_cast<uint8_t *>(table_entry(a.dst_tab, kv * a.num_layers + layer)) +
+                static_cast<uint64_t>(uniform(static_cast<uint32_t>(id))) * a.tile_bytes;
+        } else {
+            d = a.dst_lin + (static_cast<uint64_t>(plane) * a.lin_pairs + a.lin_first + i) * a.tile_bytes;
+        }
+
+        const uint32_t row0 = chunk * a.rows_per_chunk;
+        const uint32_t first = row0 * kRowBytes + lane_off;
+        // Rows of this chunk that every lane copies whole (wavefront-uniform).
+        const uint32_t whole = full_rows > row0 ? min(a.rows_per_chunk, full_rows - row0) : 0u;
+        u32x4 r[ROWS];
+        if (whole == ROWS) {
+            // Common case: ROWS complete rows, no predication at all.
+#pragma unroll
+            for (int u = 0; u < ROWS; ++u)
+                r[u] = load16(s + first + u * kRowBytes);
+#pragma unroll
+            for (int u = 0; u < ROWS; ++u)
+                store16(d + first + u * kRowBytes, r[u]);
+        } else {
+            // Fewer rows: uniform branches for the whole rows, a lane
+            // predicate only for a final partial row of the tile.
+#pragma unroll
+            for (int u = 0; u < ROWS; ++u)
+                if (u < static_cast<int>(whole))
+                    r[u] = load16(s + first + u * kRowBytes);
+#pragma unroll
+            for (int u = 0; u < ROWS; ++u)
+                if (u < static_cast<int>(whole))
+                    store16(d + first + u * kRowBytes, r[u]);
+            const uint32_t tail = first + whole * kRowBytes;
+            if (whole < a.rows_per_chunk && row0 + whole == full_rows && tail < a.tile_bytes)
+                store16(d + tail, load16(s + tail));
+        }
+    }
+}
+
+// Decode stand-in: writes whole token slots through a block table.
+struct WriteArgs {
+    const uint64_t *tab;
+    const uint8_t *data;
+    uint32_t slot_bytes;
+    uint32_t tile_bytes;
+    uint32_t block_size;
+    uint32_t num_layers;
+    uint32_t data_tokens;  // tokens in the whole call (plane stride of data)
+    uint32_t first_token;  // this launch's first token within the call
+    uint32_t tokens;       // tokens in this launch
+    uint32_t first_slot;   // slot of this launch's first token within its block
+    int32_t ids[kInlinePairs]; // blocks this launch touches, in logical order
+};
+
+__global__ void __launch_bounds__(kThreads) write_token_slots(const WriteArgs a)
+{
+    const uint32_t items = a.tokens * 2u * a.num_layers;
+    for (uint32_t item = blockIdx.x; item < items; item += gridDim.x) {
+        const uint32_t plane = item / a.tokens;
+        const uint32_t j = item - plane * a.tokens;
+        const uint32_t layer = plane >> 1, kv = plane & 1u;
+        const uint32_t rel = a.first_slot + j;
+        const uint32_t blk = rel / a.block_size;
+        const uint32_t slot = rel - blk * a.block_size;
+        uint8_t *d = reinterpret_cast<uint8_t *>(table_entry(a.tab, kv * a.num_layers + layer)) +
+                     static_cast<uint64_t>(uniform(static_cast<uint32_t>(a.ids[blk]))) * a.tile_bytes +
+                     static_cast<uint64_t>(slot) * a.slot_bytes;
+        const uint8_t *s = a.data + (static_cast<uint64_t>(plane) * a.data_tokens + a.first_token + j) *
+                                        a.slot_bytes;
+        for (uint32_t off = threadIdx.x * 16u; off < a.slot_bytes; off += kRowBytes)
+            *(LLMIG_GLOBAL u32x4 *)(d + off) = load16(s + off);
+    }
+}
+
+bool same_geometry(const llmig_pool *a, const llmig_pool *b)
+{
+    return a->num_layers == b->num_layers && a->block_size == b->block_size &&
+           a->num_kv_heads == b->num_kv_heads && a->head_dim == b->head_dim &&
+           a->elem_bytes == b->elem_bytes;
+}
+
+// Whether any layer tensor of a overlaps any of b (both span lists sorted).
+bool pools_overlap(const llmig_pool *a, const llmig_pool *b)
+{
+    if (a == b)
+        return true;
+    size_t i = 0, j = 0;
+    while (i < a->spans.size() && j < b->spans.size()) {
+        const auto &x = a->spans[i];
+        const auto &y = b->spans[j];
+        if (x.first < y.second && y.first < x.second)
+            return true;
+        if (x.second <= y.second)
+            ++i;
+        else
+            ++j;
+    }
+    return false;
+}
+
+int check_ids(const int32_t *ids, int64_t n, int32_t num_blocks)
+{
+    for (int64_t k = 0; k < n; ++k)
+        if (ids[k] < 0 || ids[k] >= num_blocks)
+            return LLMIG_ERANGE;
+    return LLMIG_OK;
+}
+
+// Whether ids[0..n) holds a repeat; ids are known to lie in [0, num_blocks).
+bool has_repeat(const int32_t *ids, int64_t n, int32_t num_blocks)
+{
+    if (n <= 32) {
+        for (int64_t a = 0; a < n; ++a)
+            for (int64_t b = a + 1; b < n; ++b)
+                if (ids[a] == ids[b])
+                    return true;
+        return false;
+    }
+    std::vector<uint8_t> seen(static_cast<size_t>(num_blocks), 0);
+    for (int64_t k = 0; k < n; ++k) {
+        if (seen[ids[k]])
+            return true;
+        seen[ids[k]] = 1;
+    }
+    return false;
+}
+
+// Whether ids[0..n) holds a repeat, for ids of any size (sorts a copy).
+bool has_repeat_any(const int32_t *ids, int64_t n)
+{
+    if (n <= 32)
+        return has_repeat(ids, n, 0);
+    std::vector<int32_t> v(ids, ids + n);
+    std::sort(v.begin(), v.end());
+    return std::adjacent_find(v.begin(), v.end()) != v.end();
+}
+
+// Row split of one tile: rows of kRowBytes, chunks of at most max_rows
+// rows, balanced so every chunk of a tile carries nearly the same number.
+void split_tile(uint32_t tile_bytes, uint32_t max_rows, uint32_t *chunks, uint32_t *rows_per_chunk)
+{
+    const uint32_t rows = (tile_bytes + kRowBytes - 1) / kRowBytes;
+    const uint32_t c = (rows + max_rows - 1) / max_rows;
+    *chunks = c;
+    *rows_per_chunk = (rows + c - 1) / c;
+}
+
+uint32_t compute_units()
+{
+    static const uint32_t cus = [] {
+        int dev = 0, n = 256;
+        if (hipGetDevice(&dev) != hipSuccess ||
+            hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
+            n = 256;
+        return static_cast<uint32_t>(n);
+    }();
+    return cus;
+}
+
+// A resident grid of 16 workgroups per CU keeps the chip busy; more items
+// than that are walked by the grid-stride loop.
+uint32_t grid_for(uint32_t items)
+{
+    return std::min(items, compute_units() * 16u);
+}
+
+template <int SRC, int DST>
+const void *copy_kernel(bool ids_on_device, bool bulk)
+{
+    if (ids_on_device)
+        return bulk ? reinterpret_cast<const void *>(&copy_tiles<SRC, DST, false, kBulkRows>)
+                    : reinterpret_cast<const void *>(&copy_tiles<SRC, DST, false, kSmallRows>);
+    return bulk ? reinterpret_cast<const void *>(&copy_tiles<SRC, DST, true, kBulkRows>)
+                : reinterpret_cast<const void *>(&copy_tiles<SRC, DST, true, kSmallRows>);
+}
+
+template <int SRC, int DST>
+int launch_copy(CopyArgs a, const int32_t *src_ids, const int32_t *dst_ids, int64_t n,
+                bool ids_on_device, hipStream_t stream)
+{
+    // Bulk copies take chunks of kBulkRows rows (most bytes in flight per
+    // lane); small ones, such as a final stage, take kSmallRows-row chunks so
+    // their few tiles spread over more CUs and finish sooner.
+    uint32_t chunks = 0, rpc = 0;
+    split_tile(a.tile_bytes, kBulkRows, &chunks, &rpc);
+    const uint64_t pairs_first_launch =
+        std::min<int64_t>(n, ids_on_device ? n : static_cast<int64_t>(kInlinePairs));
+    const bool bulk = pairs_first_launch * 2ull * a.num_layers * chunks >= kBulkItemsPerCU * compute_units();
+    if (!bulk)
+        split_tile(a.tile_bytes, kSmallRows, &chunks, &rpc);
+    a.chunks_per_tile = chunks;
+    a.rows_per_chunk = rpc;
+    const uint64_t items_per_pair = 2ull * a.num_layers * a.chunks_per_tile;
+    uint64_t per_launch = ids_on_device ? (0x7fffffffull / items_per_pair) : kInlinePairs;
+    if (per_launch == 0)
+        return LLMIG_EINVAL;
+    a.lin_pairs = static_cast<uint32_t>(n);
+    const void *fn = copy_kernel<SRC, DST>(ids_on_device, bulk);
+    for (int64_t first = 0; first < n; first += static_cast<int64_t>(per_launch)) {
+        const uint32_t m = static_cast<uint32_t>(std::min<int64_t>(n - first, per_launch));
+        a.pairs = m;
+        a.lin_first = static_cast<uint32_t>(first);
+        a.items = static_cast<uint32_t>(m * items_per_pair);
+        if (ids_on_device) {
+            a.src_ids_dev = src_ids ? src_ids + first : nullptr;
+            a.dst_ids_dev = dst_ids ? dst_ids + first : nullptr;
+        } else {
+            if (src_ids)
+                std::memcpy(a.src_ids, src_ids + first, m * sizeof(int32_t));
+            if (dst_ids)
+                std::memcpy(a.dst_ids, dst_ids + first, m * sizeof(int32_t));
+        }
+        void *args[] = {&a};
+        hipError_t e = hipLaunchKernel(fn, dim3(grid_for(a.items)), dim3(kThreads), args, 0, stream);
+        if (e != hipSuccess)
+            return hip_error(e);
+    }
+    return LLMIG_OK;
+}
+
+// Device-visible address of a staging buffer: device memory as is, pinned
+// host memory through its device mapping.  Pageable memory is refused.
+int staging_pointer(const void *p, void **out)
+{
+    hipPointerAttribute_t attr;
+    std::memset(&attr, 0, sizeof(attr));
+    hipError_t e = hipPointerGetAttributes(&attr, p);
+    if (e != hipSuccess) {
+        (void)hipGetLastError();
+        return LLMIG_EINVAL;
+    }
+    if (attr.type == hipMemoryTypeDevice) {
+        *out = const_cast<void *>(p);
+        return LLMIG_OK;
+    }
+    if (attr.type == hipMemoryTypeHost && attr.devicePointer != nullptr) {
+        *out = attr.devicePointer;
+        return LLMIG_OK;
+    }
+    return LLMIG_EINVAL;
+}
+
+int fused_copy_checks(const llmig_pool *pool, const int32_t *blocks, int64_t n, int map_on_device,
+                      const void *staging, int64_t staging_bytes, bool reject_repeats)
+{
+    if (!pool || n < 0 || (map_on_device != 0 && map_on_device != 1))
+        return LLMIG_EINVAL;
+    if (n == 0)
+        return LLMIG_OK;
+    if (!blocks || !staging || (reinterpret_cast<uintptr_t>(staging) & 15u))
+        return LLMIG_EINVAL;
+    const int64_t need = n * pool->num_layers * 2 * pool->tile_bytes;
+    if (n > (INT64_MAX / 2) / pool->num_layers / pool->tile_bytes || staging_bytes < need)
+        return LLMIG_EINVAL;
+    if (!map_on_device) {
+        int rc = check_ids(blocks, n, pool->num_blocks);
+        if (rc != LLMIG_OK)
+            return rc;
+        if (reject_repeats && has_repeat(blocks, n, pool->num_blocks))
+            return LLMIG_EINVAL;
+    }
+    return LLMIG_OK;
+}
+
+} // namespace
+
+extern "C" {
+
+int llmig_pool_create(const llmig_pool_desc *desc, llmig_pool **out)
+{
+    if (!out)
+        return LLMIG_EINVAL;
+    *out = nullptr;
+    if (!desc || desc->num_layers <= 0 || desc->num_blocks <= 0 || desc->block_size <= 0 ||
+        desc->num_kv_heads <= 0 || desc->head_dim <= 0 || desc->elem_bytes <= 0 || !desc->k_ptrs ||
+        !desc->v_ptrs)
+        return LLMIG_EINVAL;
+    const int64_t tile = static_cast<int64_t>(desc->block_size) * desc->num_kv_heads * desc->head_dim *
+                         desc->elem_bytes;
+    if (tile % 16 != 0 || tile > 0x7fffffffLL)
+        return LLMIG_EINVAL;
+    const int32_t L = desc->num_layers;
+    std::vector<uint64_t> tab(2 * static_cast<size_t>(L));
+    for (int32_t l = 0; l < L; ++l) {
+        tab[l] = desc->k_ptrs[l];
+        tab[L + l] = desc->v_ptrs[l];
+    }
+    for (uint64_t p : tab)
+        if (p == 0 || (p & 15u))
+            return LLMIG_EINVAL;
+
+    llmig_pool *pool = new (std::nothrow) llmig_pool();
+    if (!pool)
+        return LLMIG_EINVAL;
+    pool->num_layers = L;
+    pool->num_blocks = desc->num_blocks;
+    pool->block_size = desc->block_size;
+    pool->num_kv_heads = desc->num_kv_heads;
+    pool->head_dim = desc->head_dim;
+    pool->elem_bytes = desc->elem_bytes;
+    pool->tile_bytes = tile;
+    const uint64_t tensor_bytes = static_cast<uint64_t>(tile) * static_cast<uint64_t>(desc->num_blocks);
+    for (uint64_t p : tab)
+        pool->spans.emplace_back(p, p + tensor_bytes);
+    std::sort(pool->spans.begin(), pool->spans.end());
+    for (size_t k = 1; k < pool->spans.size(); ++k) {
+        if (pool->spans[k].first < pool->spans[k - 1].second) { // layer tensors overlap each other
+            delete pool;
+            return LLMIG_EINVAL;
+        }
+    }
+    hipError_t e = hipGetDevice(&pool->device);
+    if (e == hipSuccess)
+        e = hipMalloc(reinterpret_cast<void **>(&pool->d_tab), tab.size() * sizeof(uint64_t));
+    if (e == hipSuccess)
+        e = hipMemcpy(pool->d_tab, tab.data(), tab.size() * sizeof(uint64_t), hipMemcpyHostToDevice);
+    if (e != hipSuccess) {
+        if (pool->d_tab)
+            (void)hipFree(pool->d_tab);
+        delete pool;
+        return hip_error(e);
+    }
+    *out = pool;
+    return LLMIG_OK;
+}
+
+void llmig_pool_destroy(llmig_pool *pool)
+{
+    if (!pool)
+        return;
+    if (pool->d_tab)
+        (void)hipFree(pool->d_tab);
+    delete pool;
+}
+
+int64_t llmig_pool_tile_bytes(const llmig_pool *pool)
+{
+    return pool ? pool->tile_bytes : -1;
+}
+
+int llmig_plan(const int32_t *src_table, int64_t src_table_len, const int32_t *dst_free_list,
+               int64_t dst_free_len, int64_t len, int64_t from_tok, int64_t to_tok, int32_t block_size,
+               int32_t *out_src, int32_t *out_dst, int64_t out_cap, int64_t *out_n)
+{
+    if (!out_n)
+        return LLMIG_EINVAL;
+    *out_n = 0;
+    if (block_size < 1 || len < 0 || from_tok < 0 || from_tok > to_tok || to_tok > len)
+        return LLMIG_EINVAL;
+    if (from_tok % block_size != 0 || (to_tok % block_size != 0 && to_tok != len))
+        return LLMIG_EINVAL;
+    if (src_table_len < 0 || dst_free_len < 0 || out_cap < 0)
+        return LLMIG_EINVAL;
+    const int64_t blocks_of_len = len / block_size + (len % block_size != 0);
+    if (src_table_len < blocks_of_len || (blocks_of_len > 0 && !src_table))
+        return LLMIG_EINVAL;
+    const int64_t first = from_tok / block_size;
+    const int64_t n = to_tok / block_size + (to_tok % block_size != 0) - first;
+    if (n > dst_free_len)
+        return LLMIG_ENOSPC;
+    if (n > out_cap || (n > 0 && (!dst_free_list || !out_src || !out_dst)))
+        return LLMIG_EINVAL;
+    const int32_t *src = src_table + first;
+    for (int64_t k = 0; k < n; ++k)
+        if (src[k] < 0 || dst_free_list[k] < 0)
+            return LLMIG_ERANGE;
+    if (has_repeat_any(src, n) || has_repeat_any(dst_free_list, n))
+        return LLMIG_EINVAL;
+    std::memcpy(out_src, src, static_cast<size_t>(n) * sizeof(int32_t));
+    std::memcpy(out_dst, dst_free_list, static_cast<size_t>(n) * sizeof(int32_t));
+    *out_n = n;
+    return LLMIG_OK;
+}
+
+int llmig_stage(const llmig_pool *src, const llmig_pool *dst, const int32_t *map_src,
+                const int32_t *map_dst, int64_t n, int map_on_device, void *stream)
+{
+    if (!src || !dst || n < 0 || (map_on_device != 0 && map_on_device != 1))
+        return LLMIG_EINVAL;
+    if (!same_geometry(src, dst) || src->device != dst->device || pools_overlap(src, dst))
+        return LLMIG_EINVAL;
+    if (n == 0)
+        return LLMIG_OK;
+    if (!map_src || !map_dst)
+        return LLMIG_EINVAL;
+    if (!map_on_device) {
+        int rc = check_ids(map_src, n, src->num_blocks);
+        if (rc == LLMIG_OK)
+            rc = check_ids(map_dst, n, dst->num_blocks);
+        if (rc != LLMIG_OK)
+            return rc;
+        if (has_repeat(map_dst, n, dst->num_blocks))
+            return LLMIG_EINVAL;
+    }
+    CopyArgs a;
+    std::memset(&a, 0, sizeof(a));
+    a.src_tab = src->d_tab;
+    a.dst_tab = dst->d_tab;
+    a.tile_bytes = static_cast<uint32_t>(src->tile_bytes);
+    a.num_layers = static_cast<uint32_t>(src->num_layers);
+    return launch_copy<kPool, kPool>(a, map_src, map_dst, n, map_on_device != 0,
+                                     static_cast<hipStream_t>(stream));
+}
+
+int llmig_pack(const llmig_pool *src, const int32_t *blocks, int64_t n, int map_on_device,
+               void *staging, int64_t staging_bytes, void *stream)
+{
+    int rc = fused_copy_checks(src, blocks, n, map_on_device, staging, staging_bytes, false);
+    if (rc != LLMIG_OK || n == 0)
+        return rc;
+    void *lin = nullptr;
+    rc = staging_pointer(staging, &lin);
+    if (rc != LLMIG_OK)
+        return rc;
+    CopyArgs a;
+    std::memset(&a, 0, sizeof(a));
+    a.src_tab = src->d_tab;
+    a.dst_lin = static_cast<uint8_t *>(lin);
+    a.tile_bytes = static_cast<uint32_t>(src->tile_bytes);
+    a.num_layers = static_cast<uint32_t>(src->num_layers);
+    return launch_copy<kPool, kLinear>(a, blocks, nullptr, n, map_on_device != 0,
+                                       static_cast<hipStream_t>(stream));
+}
+
+int llmig_unpack(const llmig_pool *dst, const int32_t *blocks, int64_t n, int map_on_device,
+                 const void *staging, int64_t staging_bytes, void *stream)
+{
+    int rc = fused_copy_checks(dst, blocks, n, map_on_device, staging, staging_bytes, true);
+    if (rc != LLMIG_OK || n == 0)
+        return rc;
+    void *lin = nullptr;
+    rc = staging_pointer(staging, &lin);
+    if (rc != LLMIG_OK)
+        return rc;
+    CopyArgs a;
+    std::memset(&a, 0, sizeof(a));
+    a.dst_tab = dst->d_tab;
+    a.src_lin = static_cast<const uint8_t *>(lin);
+    a.tile_bytes = static_cast<uint32_t>(dst->tile_bytes);
+    a.num_layers = static_cast<uint32_t>(dst->num_layers);
+    return launch_copy<kLinear, kPool>(a, nullptr, blocks, n, map_on_device != 0,
+                                       static_cast<hipStream_t>(stream));
+}
+
+int llmig_write_tokens(const llmig_pool *pool, const int32_t *table, int64_t table_len, int64_t from_tok,
+                       int64_t n_tok, const void *data, void *stream)
+{
+    if (!pool || from_tok < 0 || n_tok < 0 || table_len < 0)
+        return LLMIG_EINVAL;
+    if (n_tok == 0)
+        return LLMIG_OK;
+    const int64_t slot_bytes = pool->tile_bytes / pool->block_size;
+    if (!table || !data || (reinterpret_cast<uintptr_t>(data) & 15u) || slot_bytes % 16 != 0 ||
+        n_tok > 0x7fffffffLL / (2 * pool->num_layers))
+        return LLMIG_EINVAL;
+    const int64_t bs = pool->block_size;
+    const int64_t first_blk = from_tok / bs, last_blk = (from_tok + n_tok - 1) / bs;
+    if (last_blk >= table_len)
+        return LLMIG_EINVAL;
+    int rc = check_ids(table + first_blk, last_blk - first_blk + 1, pool->num_blocks);
+    if (rc != LLMIG_OK)
+        return rc;
+    WriteArgs a;
+    std::memset(&a, 0, sizeof(a));
+    a.tab = pool->d_tab;
+    a.data = static_cast<const uint8_t *>(data);
+    a.slot_bytes = static_cast<uint32_t>(slot_bytes);
+    a.tile_bytes = static_cast<uint32_t>(pool->tile_bytes);
+    a.block_size = static_cast<uint32_t>(bs);
+    a.num_layers = static_cast<uint32_t>(pool->num_layers);
+    a.data_tokens = static_cast<uint32_t>(n_tok);
+    // Each launch covers whole blocks' worth of tokens, at most kInlinePairs blocks.
+    int64_t t = from_tok;
+    while (t < from_tok + n_tok) {
+        const int64_t blk0 = t / bs;
+        const int64_t end = std::min(from_tok + n_tok, (blk0 + kInlinePairs) * bs);
+        a.first_token = static_cast<uint32_t>(t - from_tok);
+        a.tokens = static_cast<uint32_t>(end - t);
+        a.first_slot = static_cast<uint32_t>(t - blk0 * bs);
+        const int64_t nblk = (end - 1) / bs - blk0 + 1;
+        std::memcpy(a.ids, table + blk0, static_cast<size_t>(nblk) * sizeof(int32_t));
+        void *args[] = {&a};
+        const uint32_t items = a.tokens * 2u * a.num_layers;
+        hipError_t e = hipLaunchKernel(reinterpret_cast<const void *>(&write_token_slots),
+                                       dim3(grid_for(items)), dim3(kThreads), args, 0,
+                                       static_cast<hipStream_t>(stream));
+        if (e != hipSuccess)
+            return hip_error(e);
+        t = end;
+    }
+    return LLMIG_OK;
+}
+
+const char *llmig_strerror(int code)
+{
+    switch (code) {
+    case LLMIG_OK:
+        return "ok";
+    case LLMIG_EINVAL:
+        return "invalid argument";
+    case LLMIG_ENOSPC:
+        return "destination free list cannot hold the stage";
+    case LLMIG_ERANGE:
+        return "block id out of range";
+    case LLMIG_EHIP:
+        return "HIP runtime error";
+    default:
+        return "unknown error";
+    }
+}
+
+int llmig_last_hip_error(void)
+{
+    return g_last_hip_error;
+}
+
+} // extern "C"

@@ -1,0 +1,219 @@
+"""Python binding of the llmig C ABI (include/llmig.h).
+
+Argument marshalling only: every step of a migration runs in the HIP library
+``libllmig.so``.  PyTorch supplies device memory, pinned host memory and
+streams; the functions take torch tensors and numpy arrays and pass their
+addresses to the library.  Importing this module without the built library
+raises ImportError: there is no fallback.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+import numpy as np
+import torch
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIBRARY = os.path.join(HERE, "libllmig.so")
+
+if not os.path.exists(LIBRARY):
+    raise ImportError(f"{LIBRARY} is not built; run __graft_entry__.build() first")
+
+_lib = ctypes.CDLL(LIBRARY)
+
+LLMIG_OK, LLMIG_EINVAL, LLMIG_ENOSPC, LLMIG_ERANGE, LLMIG_EHIP = 0, -1, -2, -3, -4
+ERROR_NAMES = {0: "OK", -1: "EINVAL", -2: "ENOSPC", -3: "ERANGE", -4: "EHIP"}
+
+
+class LlmigError(RuntimeError):
+    def __init__(self, code: int, where: str):
+        self.code = code
+        self.name = ERROR_NAMES.get(code, str(code))
+        detail = _lib.llmig_strerror(code).decode()
+        if code == LLMIG_EHIP:
+            detail += f" (hipError_t {_lib.llmig_last_hip_error()})"
+        super().__init__(f"{where}: {self.name}: {detail}")
+
+
+class _PoolDesc(ctypes.Structure):
+    _fields_ = [("num_layers", ctypes.c_int32), ("num_blocks", ctypes.c_int32),
+                ("block_size", ctypes.c_int32), ("num_kv_heads", ctypes.c_int32),
+                ("head_dim", ctypes.c_int32), ("elem_bytes", ctypes.c_int32),
+                ("k_ptrs", ctypes.POINTER(ctypes.c_uint64)), ("v_ptrs", ctypes.POINTER(ctypes.c_uint64))]
+
+
+_i32p = ctypes.POINTER(ctypes.c_int32)
+_i64p = ctypes.POINTER(ctypes.c_int64)
+_vp = ctypes.c_void_p
+
+_lib.llmig_pool_create.argtypes = [ctypes.POINTER(_PoolDesc), ctypes.POINTER(_vp)]
+_lib.llmig_pool_create.restype = ctypes.c_int
+_lib.llmig_pool_destroy.argtypes = [_vp]
+_lib.llmig_pool_destroy.restype = None
+_lib.llmig_pool_tile_bytes.argtypes = [_vp]
+_lib.llmig_pool_tile_bytes.restype = ctypes.c_int64
+_lib.llmig_plan.argtypes = [_vp, ctypes.c_int64, _vp, ctypes.c_int64, ctypes.c_int64, ctypes.c_int64,
+                            ctypes.c_int64, ctypes.c_int32, _vp, _vp, ctypes.c_int64, _i64p]
+_lib.llmig_plan.restype = ctypes.c_int
+_lib.llmig_stage.argtypes = [_vp, _vp, _vp, _vp, ctypes.c_int64, ctypes.c_int, _vp]
+_lib.llmig_stage.restype = ctypes.c_int
+_lib.llmig_pack.argtypes = [_vp, _vp, ctypes.c_int64, ctypes.c_int, _vp, ctypes.c_int64, _vp]
+_lib.llmig_pack.restype = ctypes.c_int
+_lib.llmig_unpack.argtypes = [_vp, _vp, ctypes.c_int64, ctypes.c_int, _vp, ctypes.c_int64, _vp]
+_lib.llmig_unpack.restype = ctypes.c_int
+_lib.llmig_write_tokens.argtypes = [_vp, _vp, ctypes.c_int64, ctypes.c_int64, ctypes.c_int64, _vp, _vp]
+_lib.llmig_write_tokens.restype = ctypes.c_int
+_lib.llmig_strerror.argtypes = [ctypes.c_int]
+_lib.llmig_strerror.restype = ctypes.c_char_p
+_lib.llmig_last_hip_error.argtypes = []
+_lib.llmig_last_hip_error.restype = ctypes.c_int
+
+
+def _check(code: int, where: str) -> None:
+    if code != LLMIG_OK:
+        raise LlmigError(code, where)
+
+
+def _stream(stream) -> int:
+    if stream is None:
+        return torch.cuda.current_stream().cuda_stream
+    if isinstance(stream, int):
+        return stream
+    return stream.cuda_stream
+
+
+def _host_i32(a) -> np.ndarray:
+    return np.ascontiguousarray(np.asarray(a, dtype=np.int32))
+
+
+def _ids(a):
+    """(pointer, length, on_device, keepalive) for an id list: a CUDA int32
+    tensor stays on the device, anything else becomes a host int32 array."""
+    if isinstance(a, torch.Tensor) and a.is_cuda:
+        if a.dtype != torch.int32 or not a.is_contiguous():
+            raise ValueError("device id lists must be contiguous int32 tensors")
+        return a.data_ptr(), a.numel(), 1, a
+    h = _host_i32(a.cpu().numpy() if isinstance(a, torch.Tensor) else a)
+    return h.ctypes.data, h.size, 0, h
+
+
+class Pool:
+    """A registered KV block pool: per-layer K and V tensors of shape
+    [num_blocks, block_size, num_kv_heads, head_dim] on one GPU.  The tensors
+    stay owned by the caller; the handle keeps references to them."""
+
+    def __init__(self, k_layers, v_layers):
+        if len(k_layers) != len(v_layers) or not k_layers:
+            raise ValueError("need one K and one V tensor per layer")
+        t0 = k_layers[0]
+        for t in list(k_layers) + list(v_layers):
+            if (not t.is_cuda or not t.is_contiguous() or t.dim() != 4 or t.shape != t0.shape
+                    or t.dtype != t0.dtype):
+                raise ValueError("layer tensors must be contiguous CUDA tensors of one 4-D shape and dtype")
+        nb, bs, heads, dim = t0.shape
+        kp = (ctypes.c_uint64 * len(k_layers))(*[t.data_ptr() for t in k_layers])
+        vp = (ctypes.c_uint64 * len(v_layers))(*[t.data_ptr() for t in v_layers])
+        desc = _PoolDesc(len(k_layers), nb, bs, heads, dim, t0.element_size(),
+                         ctypes.cast(kp, ctypes.POINTER(ctypes.c_uint64)),
+                         ctypes.cast(vp, ctypes.POINTER(ctypes.c_uint64)))
+        handle = _vp()
+        _check(_lib.llmig_pool_create(ctypes.byref(desc), ctypes.byref(handle)), "llmig_pool_create")
+        self._handle = handle
+        self.k, self.v = list(k_layers), list(v_layers)
+        self.num_layers, self.num_blocks, self.block_size = len(k_layers), nb, bs
+        self.num_kv_heads, self.head_dim, self.elem_bytes = heads, dim, t0.element_size()
+        self.tile_bytes = _lib.llmig_pool_tile_bytes(handle)
+        self.slot_bytes = self.tile_bytes // bs
+
+    @property
+    def handle(self):
+        if self._handle is None:
+            raise ValueError("pool is closed")
+        return self._handle
+
+    def close(self) -> None:
+        if getattr(self, "_handle", None) is not None:
+            _lib.llmig_pool_destroy(self._handle)
+            self._handle = None
+
+    def __del__(self):
+        self.close()
+
+
+def llmig_plan(src_table, dst_free_list, length, from_tok, to_tok, block_size, out_cap=None):
+    """Plan one stage; returns (map_src, map_dst) as host int32 arrays."""
+    st, fl = _host_i32(src_table), _host_i32(dst_free_list)
+    cap = len(fl) if out_cap is None else int(out_cap)
+    out_s = np.empty(max(cap, 1), np.int32)
+    out_d = np.empty(max(cap, 1), np.int32)
+    n = ctypes.c_int64(0)
+    _check(_lib.llmig_plan(st.ctypes.data, st.size, fl.ctypes.data, fl.size, int(length), int(from_tok),
+                           int(to_tok), int(block_size), out_s.ctypes.data, out_d.ctypes.data, cap,
+                           ctypes.byref(n)), "llmig_plan")
+    return out_s[:n.value], out_d[:n.value]
+
+
+def llmig_plan_code(src_table, dst_free_list, length, from_tok, to_tok, block_size, out_cap=None,
+                    sentinel=None):
+    """Raw form of :func:`llmig_plan` for tests: returns (code, out_src,
+    out_dst, n) with the full output arrays (pre-filled with ``sentinel``)."""
+    st, fl = _host_i32(src_table), _host_i32(dst_free_list)
+    cap = len(fl) if out_cap is None else int(out_cap)
+    out_s = np.full(max(cap, 1), -7 if sentinel is None else sentinel, np.int32)
+    out_d = out_s.copy()
+    n = ctypes.c_int64(-1)
+    code = _lib.llmig_plan(st.ctypes.data, st.size, fl.ctypes.data, fl.size, int(length), int(from_tok),
+                           int(to_tok), int(block_size), out_s.ctypes.data, out_d.ctypes.data, cap,
+                           ctypes.byref(n))
+    return code, out_s, out_d, n.value
+
+
+def llmig_stage(src: Pool, dst: Pool, map_src, map_dst, stream=None) -> None:
+    """Enqueue one pool-to-pool stage.  Host id arrays travel inside the
+    kernel arguments; CUDA int32 tensors are read on the device."""
+    ps, ns, ds, ks = _ids(map_src)
+    pd, nd, dd, kd = _ids(map_dst)
+    if ns != nd or ds != dd:
+        raise ValueError("map_src and map_dst must have one length and one location")
+    _check(_lib.llmig_stage(src.handle, dst.handle, ps, pd, ns, ds, _stream(stream)), "llmig_stage")
+
+
+def _staging(staging: torch.Tensor):
+    if not staging.is_contiguous():
+        raise ValueError("staging must be contiguous")
+    if not staging.is_cuda and not staging.is_pinned():
+        raise ValueError("host staging must be pinned memory")
+    return staging.data_ptr(), staging.numel() * staging.element_size()
+
+
+def llmig_pack(src: Pool, blocks, staging: torch.Tensor, stream=None) -> None:
+    """Gather the listed blocks into staging laid out [L][K,V][n][tile]."""
+    pb, n, on_dev, keep = _ids(blocks)
+    ptr, nbytes = _staging(staging)
+    _check(_lib.llmig_pack(src.handle, pb, n, on_dev, ptr, nbytes, _stream(stream)), "llmig_pack")
+
+
+def llmig_unpack(dst: Pool, blocks, staging: torch.Tensor, stream=None) -> None:
+    """Scatter a buffer laid out as llmig_pack writes it into the listed blocks."""
+    pb, n, on_dev, keep = _ids(blocks)
+    ptr, nbytes = _staging(staging)
+    _check(_lib.llmig_unpack(dst.handle, pb, n, on_dev, ptr, nbytes, _stream(stream)), "llmig_unpack")
+
+
+def llmig_write_tokens(pool: Pool, table, from_tok: int, data: torch.Tensor, stream=None) -> None:
+    """Decode stand-in: write tokens [from_tok, from_tok + n_tok) through
+    ``table``; data is a CUDA tensor laid out [L][K,V][n_tok][slot_bytes]."""
+    if not data.is_cuda or not data.is_contiguous():
+        raise ValueError("data must be a contiguous CUDA tensor")
+    nbytes = data.numel() * data.element_size()
+    per_tok = pool.num_layers * 2 * pool.slot_bytes
+    if nbytes % per_tok:
+        raise ValueError("data size is not a whole number of tokens")
+    t = _host_i32(table)
+    _check(_lib.llmig_write_tokens(pool.handle, t.ctypes.data, t.size, int(from_tok), nbytes // per_tok,
+                                   data.data_ptr(), _stream(stream)), "llmig_write_tokens")
+
+
+def exported_symbols():
+    return _lib

@@ -1,0 +1,168 @@
+"""Multi-stage live migration of one request (Llumnix §4.2), driven over the
+llmig C ABI.
+
+Stage 0 copies every block the request has filled so far while decoding goes
+on; each later stage copies the blocks filled during the previous stage; once
+little enough is left, the request is drained from its batch and a final
+stage copies the rest, partial last block included.  Only that final stage is
+downtime.  Non-final stages copy whole blocks only: a block still being
+appended to is left for a later stage, which is also what makes the copy
+race-free against decoding's writes (blocks already copied are never written
+again, because the KV cache is append-only).
+
+The copies run on a migration stream of their own; decoding's KV writes run on
+a decode stream; an event recorded after each batch of writes orders the next
+stage after them.  All streams keep the default priority.
+"""
+from __future__ import annotations
+
+import math
+import time
+from dataclasses import dataclass, field
+
+import numpy as np
+import torch
+
+from .llmig import Pool, llmig_plan, llmig_stage, llmig_write_tokens
+
+
+@dataclass
+class StageRecord:
+    length: int        # tokens resident when the stage was planned
+    from_tok: int
+    to_tok: int
+    blocks: int
+    final: bool
+    gpu_us: float = 0.0
+    map_src: np.ndarray = field(default=None, repr=False)
+    map_dst: np.ndarray = field(default=None, repr=False)
+
+
+class Migration:
+    """Bookkeeping of one request's migration: which tokens are copied, which
+    destination blocks were reserved, and the stages so far."""
+
+    def __init__(self, src: Pool, dst: Pool, src_table, dst_free_list, stream: torch.cuda.Stream):
+        self.src, self.dst, self.stream = src, dst, stream
+        self.bs = src.block_size
+        self.src_table = np.ascontiguousarray(np.asarray(src_table, dtype=np.int32))
+        self.free = np.ascontiguousarray(np.asarray(dst_free_list, dtype=np.int32))
+        self.copied_tok = 0
+        self.dst_table: list[int] = []
+        self.stages: list[StageRecord] = []
+        self._events = []
+
+    def remaining_blocks(self, length: int) -> int:
+        return math.ceil(length / self.bs) - self.copied_tok // self.bs
+
+    def stage(self, length: int, final: bool, time_it: bool = True) -> StageRecord:
+        """Plan and launch the next stage for a request that now holds
+        ``length`` tokens.  A non-final stage stops at the last whole block."""
+        end = length if final else (length // self.bs) * self.bs
+        ms, md = llmig_plan(self.src_table, self.free, length, self.copied_tok, end, self.bs)
+        ev = None
+        if time_it:
+            ev = (torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+            ev[0].record(self.stream)
+        llmig_stage(self.src, self.dst, ms, md, stream=self.stream)
+        if time_it:
+            ev[1].record(self.stream)
+        rec = StageRecord(length, self.copied_tok, end, len(md), final, map_src=ms, map_dst=md)
+        self.stages.append(rec)
+        self._events.append(ev)
+        self.free = self.free[len(md):]
+        self.dst_table.extend(int(x) for x in md)
+        self.copied_tok = end
+        return rec
+
+    def collect_times(self) -> None:
+        """Fill in each stage's GPU time (call after the stream is synchronised)."""
+        for rec, ev in zip(self.stages, self._events):
+            if ev is not None:
+                rec.gpu_us = ev[0].elapsed_time(ev[1]) * 1e3
+
+
+def run_scheduled(src: Pool, dst: Pool, src_table, dst_free_list, initial_len: int, appends,
+                  mig_stream, dec_stream):
+    """A migration whose decoding appends a known batch of tokens before each
+    incremental stage (``appends`` is a list of device tensors laid out
+    [L][K,V][n_tok][slot_bytes]); the stage after the last batch is final.
+    Returns (migration, downtime_us): downtime is host wall time from the
+    start of the final stage's planning until the host sees it complete."""
+    m = Migration(src, dst, src_table, dst_free_list, mig_stream)
+    length = initial_len
+    ready = torch.cuda.Event()
+    ready.record(dec_stream)
+    mig_stream.wait_event(ready)
+    m.stage(length, final=not appends)
+    downtime_us = None
+    for k, data in enumerate(appends):
+        n_tok = data.numel() // (src.num_layers * 2 * src.slot_bytes)
+        llmig_write_tokens(src, src_table, length, data, stream=dec_stream)
+        length += n_tok
+        ev = torch.cuda.Event()
+        ev.record(dec_stream)
+        final = k == len(appends) - 1
+        if final:
+            # The final stage starts once the previous stage's copy is done
+            # and the request is drained (its last token written).
+            mig_stream.synchronize()
+            ev.synchronize()
+            t0 = time.perf_counter()
+            mig_stream.wait_event(ev)
+            m.stage(length, final=True, time_it=False)
+            mig_stream.synchronize()
+            downtime_us = (time.perf_counter() - t0) * 1e6
+        else:
+            mig_stream.wait_event(ev)
+            m.stage(length, final=False)
+    if downtime_us is None:
+        t0 = time.perf_counter()
+        mig_stream.synchronize()
+        downtime_us = (time.perf_counter() - t0) * 1e6
+    m.collect_times()
+    return m, downtime_us
+
+
+def run_timed(src: Pool, dst: Pool, src_table, initial_len: int, dst_free_list, append_pool,
+              mig_stream, dec_stream, step_ms: float = 20.0, last_stage_max_blocks: int = 1,
+              max_stages: int = 8):
+    """A migration whose decoding speed is simulated: while a stage copies,
+    decoding produces max(1, ceil(stage_time / step_ms)) tokens, which are
+    written once the stage is over.  The next stage is final when at most
+    ``last_stage_max_blocks`` blocks remain, or at ``max_stages``.
+    ``append_pool`` is a device tensor [L][K,V][max_tokens][slot_bytes] the
+    appended tokens are drawn from.  Returns (migration, downtime_us)."""
+    m = Migration(src, dst, src_table, dst_free_list, mig_stream)
+    length = initial_len
+    max_tok = append_pool.shape[2]
+    used = 0
+    ready = torch.cuda.Event()
+    ready.record(dec_stream)
+    mig_stream.wait_event(ready)
+    rec = m.stage(length, final=False)
+    while True:
+        mig_stream.synchronize()
+        m.collect_times()
+        n_tok = max(1, math.ceil(rec.gpu_us / (step_ms * 1e3)))
+        if used + n_tok > max_tok:
+            raise RuntimeError("append pool exhausted")
+        with torch.cuda.stream(dec_stream):
+            data = append_pool[:, :, used:used + n_tok].contiguous()
+        llmig_write_tokens(src, src_table, length, data, stream=dec_stream)
+        used += n_tok
+        length += n_tok
+        ev = torch.cuda.Event()
+        ev.record(dec_stream)
+        if m.remaining_blocks(length) <= last_stage_max_blocks or len(m.stages) + 1 >= max_stages:
+            ev.synchronize()
+            t0 = time.perf_counter()
+            mig_stream.wait_event(ev)
+            m.stage(length, final=True, time_it=False)
+            mig_stream.synchronize()
+            downtime_us = (time.perf_counter() - t0) * 1e6
+            break
+        mig_stream.wait_event(ev)
+        rec = m.stage(length, final=False)
+    m.collect_times()
+    return m, downtime_us

@@ -1,0 +1,295 @@
+"""GPU parity: the HIP path against the CPU oracle, byte for byte
+(tolerance 0: a migration is a copy).  Every case runs through the C ABI.
+
+Each test prints the case it is about to run (flushed) so a failing GPU run
+names it."""
+import sys
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from oracle import HostPool
+from paper_2406_03243_amd import harness
+from paper_2406_03243_amd import workloads as wl
+
+pytestmark = pytest.mark.gpu
+
+if torch.cuda.is_available():
+    from paper_2406_03243_amd import llmig
+    from paper_2406_03243_amd.llmig import Pool, LlmigError
+    from paper_2406_03243_amd import migrate
+
+
+def say(*a):
+    print("[case]", *a, flush=True)
+    sys.stdout.flush()
+
+
+def host_image(pool) -> HostPool:
+    return HostPool(harness.snapshot(pool.k), harness.snapshot(pool.v), pool.block_size, pool.slot_bytes)
+
+
+def make_pool(shape: wl.PoolShape, seed: int, purpose: int, num_blocks=None, random_bytes=False):
+    k, v = harness.alloc_layers(shape, num_blocks=num_blocks)
+    if random_bytes:
+        total = sum(t.numel() * t.element_size() for t in k + v)
+        harness.fill_bytes_from_host(k + v, wl.random_bytes(seed, purpose, total))
+    else:
+        harness.fill_from_host(k + v, seed, purpose, shape.dtype)
+    return Pool(k, v)
+
+
+def assert_same(gpu: HostPool, want: HostPool, what: str):
+    for l in range(want.num_layers):
+        for kv, (a, b) in enumerate(((gpu.k[l], want.k[l]), (gpu.v[l], want.v[l]))):
+            if not np.array_equal(a, b):
+                bad = np.nonzero((a != b).any(axis=1))[0]
+                raise AssertionError(f"{what}: layer {l} {'KV'[kv]} differs in blocks {bad[:10].tolist()}"
+                                     f" ({len(bad)} blocks)")
+
+
+# ------------------------------------------------------------------- tiny config, exactly
+def test_tiny_single_stage():
+    w = wl.TINY
+    say("tiny single stage", w.shape)
+    src = make_pool(w.shape, w.seed, wl.SRC_VALUES)
+    dst = make_pool(w.shape, w.seed, wl.DST_VALUES)
+    table, _ = wl.request_table(w.seed, w.shape.num_blocks, w.table_blocks)
+    free, _ = wl.free_list(w.seed, w.shape.num_blocks)
+    length = w.lengths[0]
+    ms, md = llmig.llmig_plan(table, free, length, 0, length, w.shape.block_size)
+    code, oms, omd = oracle.default().plan(table, free, length, 0, length, w.shape.block_size)
+    assert code == oracle.OK and np.array_equal(ms, oms) and np.array_equal(md, omd)
+    assert len(ms) == 13
+    hs, hd = host_image(src), host_image(dst)
+    llmig.llmig_stage(src, dst, ms, md)
+    torch.cuda.synchronize()
+    oracle.default().copy(hs, hd, oms, omd)
+    assert_same(host_image(dst), hd, "destination")
+    assert_same(host_image(src), hs, "source")
+    assert oracle.default().first_token_mismatch(hs, table, host_image(dst), md, length) == -1
+
+
+# ------------------------------------------------------------------- stage: shapes, tails, launches
+STAGE_CASES = [
+    # (layers, num_blocks src, dst, block_size, heads, head_dim, pairs, ids on device)
+    (3, 700, 650, 16, 3, 64, 600, False),     # 6 KiB tiles: 1.5 rows; 3 launches of inline ids
+    (3, 700, 650, 16, 3, 64, 600, True),
+    (2, 300, 300, 16, 13, 128, 257, False),   # 52 KiB tiles: 13 rows, chunks of 7 + 6
+    (2, 64, 80, 16, 33, 128, 40, True),       # 33 rows
+    (4, 90, 90, 16, 5, 72, 77, False),        # 11.25 KiB: a partial last row
+    (2, 50, 50, 1, 1, 8, 50, False),          # 16-byte tiles
+    (1, 40, 40, 8, 1, 8, 1, False),           # 128-byte tiles, a single pair
+    (2, 600, 600, 16, 32, 128, 512, False),   # LLaMA-7B tiles (128 KiB)
+]
+
+
+@pytest.mark.parametrize("case", STAGE_CASES, ids=lambda c: "L{}_T{}_n{}_{}".format(
+    c[0], c[3] * c[4] * c[5] * 2, c[6], "dev" if c[7] else "host"))
+def test_stage_parity(case):
+    L, nbs, nbd, bs, h, d, n, dev = case
+    say("stage", case)
+    shape = wl.PoolShape(L, nbs, bs, h, d, "fp16")
+    seed = 7000 + n
+    src = make_pool(shape, seed, wl.SRC_VALUES, random_bytes=True)
+    dst = make_pool(shape, seed, wl.DST_VALUES, num_blocks=nbd, random_bytes=True)
+    g = wl.stream(seed, wl.EXTRA)
+    ms = g.choice(nbs, n, replace=False).astype(np.int32)
+    md = g.choice(nbd, n, replace=False).astype(np.int32)
+    hs, hd = host_image(src), host_image(dst)
+    if dev:
+        llmig.llmig_stage(src, dst, torch.from_numpy(ms).cuda(), torch.from_numpy(md).cuda())
+    else:
+        llmig.llmig_stage(src, dst, ms, md)
+    torch.cuda.synchronize()
+    oracle.default().copy(hs, hd, ms, md)
+    assert_same(host_image(dst), hd, "destination")
+    assert_same(host_image(src), hs, "source")
+
+
+def test_special_bit_patterns_survive():
+    say("special 16-bit patterns")
+    shape = wl.PoolShape(2, 64, 16, 4, 64, "bf16")
+    k, v = harness.alloc_layers(shape)
+    pat = wl.special_patterns16()
+    for i, t in enumerate(k + v):
+        bits = np.resize(np.roll(pat, i), t.numel())
+        t.view(torch.int16).reshape(-1).copy_(torch.from_numpy(bits.view(np.int16)))
+    src = Pool(k, v)
+    dst = make_pool(shape, 31, wl.DST_VALUES)
+    ms = np.arange(0, 64, 2, dtype=np.int32)
+    md = np.arange(63, 0, -2, dtype=np.int32)
+    hs, hd = host_image(src), host_image(dst)
+    llmig.llmig_stage(src, dst, ms, md)
+    torch.cuda.synchronize()
+    oracle.default().copy(hs, hd, ms, md)
+    assert_same(host_image(dst), hd, "destination")
+
+
+# ------------------------------------------------------------------- pack / unpack
+@pytest.mark.parametrize("where", ["device", "pinned"])
+@pytest.mark.parametrize("dev_ids", [False, True])
+def test_pack_unpack_parity(where, dev_ids):
+    say("pack/unpack", where, "device ids" if dev_ids else "host ids")
+    shape = wl.PoolShape(3, 400, 16, 5, 72, "fp16")   # ragged tiles
+    src = make_pool(shape, 41, wl.SRC_VALUES, random_bytes=True)
+    dst = make_pool(shape, 41, wl.DST_VALUES, num_blocks=380, random_bytes=True)
+    g = wl.stream(41, wl.EXTRA)
+    n = 300
+    bs_ = g.choice(400, n, replace=False).astype(np.int32)
+    bd_ = g.choice(380, n, replace=False).astype(np.int32)
+    nbytes = n * shape.num_layers * 2 * src.tile_bytes
+    if where == "device":
+        staging = torch.empty(nbytes + 64, dtype=torch.uint8, device="cuda")
+    else:
+        staging = torch.empty(nbytes + 64, dtype=torch.uint8, pin_memory=True)
+    staging.fill_(0xA5)
+    torch.cuda.synchronize()
+    ids_s = torch.from_numpy(bs_).cuda() if dev_ids else bs_
+    ids_d = torch.from_numpy(bd_).cuda() if dev_ids else bd_
+    hs, hd = host_image(src), host_image(dst)
+    llmig.llmig_pack(src, ids_s, staging)
+    torch.cuda.synchronize()
+    got = staging.cpu().numpy()
+    want = oracle.default().pack(hs, bs_)
+    assert np.array_equal(got[:nbytes], want)
+    assert (got[nbytes:] == 0xA5).all()            # nothing written past the packed bytes
+    llmig.llmig_unpack(dst, ids_d, staging)
+    torch.cuda.synchronize()
+    oracle.default().unpack(hd, bd_, want)
+    assert_same(host_image(dst), hd, "destination after unpack")
+    assert_same(host_image(src), hs, "source")
+
+
+# ------------------------------------------------------------------- multi-stage
+def _appends(shape, seed, counts, slot_bytes):
+    out = []
+    for k, c in enumerate(counts):
+        bits = wl.values16(seed, wl.APPEND_VALUES, shape.num_layers * 2 * int(c) * slot_bytes // 2,
+                           shape.dtype, sub=k)
+        out.append(bits.view(np.uint8).reshape(shape.num_layers, 2, int(c), slot_bytes))
+    return out
+
+
+def test_multistage_scheduled_small():
+    shape = wl.PoolShape(4, 300, 16, 4, 64, "fp16")
+    seed, initial, counts = 5151, 1000, [16, 33, 64, 7]
+    say("multistage scheduled", shape, initial, counts)
+    src = make_pool(shape, seed, wl.SRC_VALUES)
+    dst = make_pool(shape, seed, wl.DST_VALUES)
+    table, _ = wl.request_table(seed, shape.num_blocks, 80, 0.3)
+    free, _ = wl.free_list(seed, shape.num_blocks, 0.3)
+    data = _appends(shape, seed, counts, src.slot_bytes)
+    hs, hd = host_image(src), host_image(dst)
+    mig, dec = torch.cuda.Stream(), torch.cuda.Stream()
+    m, downtime = migrate.run_scheduled(src, dst, table, free, initial,
+                                        [torch.from_numpy(x).cuda() for x in data], mig, dec)
+    torch.cuda.synchronize()
+    bounds = oracle.stage_bounds(initial, counts, shape.block_size)
+    assert [(r.length, r.from_tok, r.to_tok) for r in m.stages] == bounds
+    events, cur = [], initial
+    for k, (length, lo, hi) in enumerate(bounds):
+        if k:
+            events.append(("append", cur, data[k - 1]))
+            cur += counts[k - 1]
+        events.append(("stage", length, lo, hi))
+    dst_table, _ = oracle.default().migrate(hs, hd, table, free, events)
+    assert np.array_equal(np.asarray(m.dst_table, np.int32), dst_table)
+    gs, gd = host_image(src), host_image(dst)
+    assert_same(gs, hs, "source (with appends)")
+    assert_same(gd, hd, "destination")
+    final_len = initial + sum(counts)
+    assert len(dst_table) == -(-final_len // shape.block_size)
+    assert oracle.default().first_token_mismatch(gs, table, gd, dst_table, final_len) == -1
+    assert downtime > 0
+
+
+def test_multistage_timed_small():
+    shape = wl.PoolShape(6, 600, 16, 13, 128, "fp16")
+    seed, initial = 6262, 4096
+    say("multistage timed", shape, initial)
+    src = make_pool(shape, seed, wl.SRC_VALUES)
+    dst = make_pool(shape, seed, wl.DST_VALUES)
+    table, _ = wl.request_table(seed, shape.num_blocks, 300)
+    free, _ = wl.free_list(seed, shape.num_blocks)
+    max_tok = 600
+    pool_bits = wl.values16(seed, wl.APPEND_VALUES, shape.num_layers * 2 * max_tok * src.slot_bytes // 2,
+                            shape.dtype)
+    append_pool = pool_bits.view(np.uint8).reshape(shape.num_layers, 2, max_tok, src.slot_bytes)
+    # load the kernels first, on throwaway pools, so no stage pays for it
+    wa = make_pool(wl.PoolShape(6, 4, 16, 13, 128, "fp16"), 1, wl.EXTRA)
+    wb = make_pool(wl.PoolShape(6, 4, 16, 13, 128, "fp16"), 2, wl.EXTRA)
+    llmig.llmig_stage(wa, wb, [0, 1], [2, 3])
+    llmig.llmig_write_tokens(wa, [0], 0, torch.zeros(6 * 2 * src.slot_bytes, dtype=torch.uint8, device="cuda"))
+    torch.cuda.synchronize()
+    hs, hd = host_image(src), host_image(dst)
+    mig, dec = torch.cuda.Stream(), torch.cuda.Stream()
+    # a very short simulated decode step forces several stages
+    m, downtime = migrate.run_timed(src, dst, table, initial, free, torch.from_numpy(append_pool).cuda(),
+                                    mig, dec, step_ms=0.005, last_stage_max_blocks=1, max_stages=6)
+    torch.cuda.synchronize()
+    # replay the recorded schedule on the host
+    events, cur, used = [], initial, 0
+    for k, r in enumerate(m.stages):
+        if r.length > cur:
+            n_tok = r.length - cur
+            events.append(("append", cur, np.ascontiguousarray(append_pool[:, :, used:used + n_tok])))
+            used += n_tok
+            cur = r.length
+        events.append(("stage", r.length, r.from_tok, r.to_tok))
+    assert m.stages[-1].final and all(not r.final for r in m.stages[:-1])
+    lo = [r.from_tok for r in m.stages]
+    hi = [r.to_tok for r in m.stages]
+    assert lo[0] == 0 and all(a == b for a, b in zip(hi[:-1], lo[1:])) and hi[-1] == cur
+    dst_table, _ = oracle.default().migrate(hs, hd, table, free, events)
+    gs, gd = host_image(src), host_image(dst)
+    assert_same(gs, hs, "source (with appends)")
+    assert_same(gd, hd, "destination")
+    assert oracle.default().first_token_mismatch(gs, table, gd, dst_table, cur) == -1
+
+
+# ------------------------------------------------------------------- errors leave no trace
+def test_errors_have_no_effect():
+    say("error paths")
+    shape = wl.PoolShape(2, 32, 16, 2, 64, "fp16")
+    src = make_pool(shape, 77, wl.SRC_VALUES)
+    dst = make_pool(shape, 77, wl.DST_VALUES)
+    other = make_pool(wl.PoolShape(2, 32, 16, 4, 64, "fp16"), 77, wl.EXTRA)
+    before = host_image(dst)
+
+    def code(fn, *a):
+        try:
+            fn(*a)
+        except LlmigError as e:
+            return e.name
+        return "OK"
+
+    assert code(llmig.llmig_stage, src, dst, [0, 1], [3, 32]) == "ERANGE"
+    assert code(llmig.llmig_stage, src, dst, [0, -1], [3, 4]) == "ERANGE"
+    assert code(llmig.llmig_stage, src, dst, [0, 1], [5, 5]) == "EINVAL"       # repeated destination
+    assert code(llmig.llmig_stage, src, src, [0], [1]) == "EINVAL"             # same pool
+    assert code(llmig.llmig_stage, src, other, [0], [1]) == "EINVAL"           # different geometry
+    alias = Pool(dst.k[::-1], dst.v[::-1])                                     # same memory, other handle
+    assert code(llmig.llmig_stage, dst, alias, [0], [1]) == "EINVAL"
+    small = torch.empty(src.tile_bytes * 4 - 16, dtype=torch.uint8, device="cuda")
+    assert code(llmig.llmig_pack, src, [0], small) == "EINVAL"                 # needs 1 * 2 * 2 tiles
+    pageable = torch.empty(src.tile_bytes * 4, dtype=torch.uint8)
+    assert code(lambda: llmig._check(llmig._lib.llmig_pack(src.handle, np.zeros(1, np.int32).ctypes.data,
+                                                           1, 0, pageable.data_ptr(),
+                                                           pageable.numel(), None), "pack")) == "EINVAL"
+    good = torch.zeros(src.tile_bytes * 4, dtype=torch.uint8, device="cuda")
+    assert code(llmig.llmig_unpack, dst, [1, 1], torch.zeros(src.tile_bytes * 8, dtype=torch.uint8,
+                                                              device="cuda")) == "EINVAL"
+    assert code(llmig.llmig_unpack, dst, [40], good) == "ERANGE"
+    data = torch.zeros(2 * 2 * 3 * src.slot_bytes, dtype=torch.uint8, device="cuda")
+    assert code(llmig.llmig_write_tokens, dst, [0], 15, data) == "EINVAL"      # table misses block 1
+    assert code(llmig.llmig_write_tokens, dst, [0, 99], 15, data) == "ERANGE"
+    torch.cuda.synchronize()
+    assert_same(host_image(dst), before, "destination after rejected calls")
+    # empty calls are fine and do nothing
+    llmig.llmig_stage(src, dst, np.zeros(0, np.int32), np.zeros(0, np.int32))
+    llmig.llmig_pack(src, np.zeros(0, np.int32), good)
+    torch.cuda.synchronize()
+    assert_same(host_image(dst), before, "destination after empty calls")
