@@ -48,9 +48,16 @@ class Migration:
         self.src_table = np.ascontiguousarray(np.asarray(src_table, dtype=np.int32))
         self.free = np.ascontiguousarray(np.asarray(dst_free_list, dtype=np.int32))
         self.copied_tok = 0
-        self.dst_table: list[int] = []
+        self._dst_parts: list[np.ndarray] = []
         self.stages: list[StageRecord] = []
         self._events = []
+
+    @property
+    def dst_table(self) -> np.ndarray:
+        """Destination block of every logical block copied so far."""
+        if not self._dst_parts:
+            return np.zeros(0, np.int32)
+        return np.concatenate(self._dst_parts)
 
     def remaining_blocks(self, length: int) -> int:
         return math.ceil(length / self.bs) - self.copied_tok // self.bs
@@ -71,7 +78,7 @@ class Migration:
         self.stages.append(rec)
         self._events.append(ev)
         self.free = self.free[len(md):]
-        self.dst_table.extend(int(x) for x in md)
+        self._dst_parts.append(md)
         self.copied_tok = end
         return rec
 
@@ -82,13 +89,22 @@ class Migration:
                 rec.gpu_us = ev[0].elapsed_time(ev[1]) * 1e3
 
 
+def wait_spin(stream) -> None:
+    """Wait for a stream by polling it: on the downtime path this returns
+    sooner after the copy ends than a blocking wait, which may sleep."""
+    while not stream.query():
+        pass
+
+
 def run_scheduled(src: Pool, dst: Pool, src_table, dst_free_list, initial_len: int, appends,
-                  mig_stream, dec_stream):
+                  mig_stream, dec_stream, time_all: bool = False):
     """A migration whose decoding appends a known batch of tokens before each
     incremental stage (``appends`` is a list of device tensors laid out
     [L][K,V][n_tok][slot_bytes]); the stage after the last batch is final.
-    Returns (migration, downtime_us): downtime is host wall time from the
-    start of the final stage's planning until the host sees it complete."""
+    Stage 0 is timed with events on the migration stream; the incremental
+    stages too when ``time_all``.  Returns (migration, downtime_us):
+    downtime is host wall time from the start of the final stage's planning
+    until the host sees it complete."""
     m = Migration(src, dst, src_table, dst_free_list, mig_stream)
     length = initial_len
     ready = torch.cuda.Event()
@@ -109,13 +125,12 @@ def run_scheduled(src: Pool, dst: Pool, src_table, dst_free_list, initial_len: i
             mig_stream.synchronize()
             ev.synchronize()
             t0 = time.perf_counter()
-            mig_stream.wait_event(ev)
             m.stage(length, final=True, time_it=False)
-            mig_stream.synchronize()
+            wait_spin(mig_stream)
             downtime_us = (time.perf_counter() - t0) * 1e6
         else:
             mig_stream.wait_event(ev)
-            m.stage(length, final=False)
+            m.stage(length, final=False, time_it=time_all)
     if downtime_us is None:
         t0 = time.perf_counter()
         mig_stream.synchronize()
@@ -157,9 +172,8 @@ def run_timed(src: Pool, dst: Pool, src_table, initial_len: int, dst_free_list, 
         if m.remaining_blocks(length) <= last_stage_max_blocks or len(m.stages) + 1 >= max_stages:
             ev.synchronize()
             t0 = time.perf_counter()
-            mig_stream.wait_event(ev)
             m.stage(length, final=True, time_it=False)
-            mig_stream.synchronize()
+            wait_spin(mig_stream)
             downtime_us = (time.perf_counter() - t0) * 1e6
             break
         mig_stream.wait_event(ev)
