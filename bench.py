@@ -66,7 +66,8 @@ def main():
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--cpu-seconds", type=float, default=10.0, help="CPU oracle sample budget")
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--no-downtime-sweep", action="store_true")
+    ap.add_argument("--sections", default="downtime,batched,load",
+                    help="extra workloads after the main one (comma list of downtime, batched, load; empty for none)")
     ap.add_argument("--downtime-reps", type=int, default=7)
     ap.add_argument("--calibration-copy", action="store_true",
                     help="end with two plain 1 GiB device-to-device copies (hardware counter calibration)")
@@ -83,31 +84,17 @@ def main():
     if not os.path.exists(LIBRARY):
         import __graft_entry__
         __graft_entry__.build()
-    from paper_2406_03243_amd import harness, migrate
-    from paper_2406_03243_amd import workloads as wl
-    from paper_2406_03243_amd.llmig import Pool
+    from paper_2406_03243_amd import migrate, scenarios
 
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
 
     # ------------------------------------------------------------------ workload
-    w = wl.LLAMA7B
-    shape = w.shape
-    log("allocating", w.name, shape)
-    sk, sv = harness.alloc_layers(shape, device=dev)
-    dk, dv = harness.alloc_layers(shape, device=dev)
-    harness.fill_on_device(sk + sv, w.seed * 16 + wl.SRC_VALUES)
-    harness.fill_on_device(dk + dv, w.seed * 16 + wl.DST_VALUES)
-    src, dst = Pool(sk, sv), Pool(dk, dv)
-    table, _ = wl.request_table(w.seed, shape.num_blocks, w.table_blocks, w.src_preoccupied)
-    free, _ = wl.free_list(w.seed, shape.num_blocks, w.dst_preoccupied)
-    counts = wl.append_counts(w.seed, w.appends, w.append_lo, w.append_hi)
-    appends = []
-    for k, c in enumerate(counts):
-        bits = wl.values16(w.seed, wl.APPEND_VALUES, shape.num_layers * 2 * int(c) * src.slot_bytes // 2,
-                           shape.dtype, sub=k)
-        appends.append(torch.from_numpy(bits.view(np.uint8)).to(dev))
-    initial = w.lengths[0]
+    su = scenarios.llama7b(dev)
+    w, shape, src, dst = su.workload, su.shape, su.src, su.dst
+    table, free, counts, appends = su.tables[0], su.free, su.counts, su.appends
+    log("allocated", w.name, shape)
+    initial = su.lengths[0]
     mig, dec = torch.cuda.Stream(device=dev), torch.cuda.Stream(device=dev)
     torch.cuda.synchronize()
 
@@ -199,16 +186,21 @@ def main():
         torch.cuda.synchronize()
         del a, b
 
-    del appends
-    src.close()
-    dst.close()
-    del sk, sv, dk, dv, src, dst
+    su.close()
+    del su, src, dst, appends
     torch.cuda.synchronize()
     torch.cuda.empty_cache()
 
-    # ------------------------------------------------------------------ downtime vs length
-    if not args.no_downtime_sweep:
+    sections = set(args.sections.split(",")) if args.sections else set()
+    if "downtime" in sections:
         result["downtime_vs_len"] = downtime_sweep(args.downtime_reps)
+        torch.cuda.empty_cache()
+    if "batched" in sections:
+        result["batched"] = batched_section()
+        torch.cuda.empty_cache()
+    if "load" in sections:
+        result["under_load"] = load_section()
+        torch.cuda.empty_cache()
 
     print(json.dumps(result), flush=True)
 
@@ -245,30 +237,19 @@ def cpu_baseline(src, stage1, shape, seconds):
 
 
 def downtime_sweep(reps):
-    import numpy as np
+    """Final-stage downtime against sequence length, LLaMA-30B quarter."""
     import torch
 
-    from paper_2406_03243_amd import harness, migrate
-    from paper_2406_03243_amd import workloads as wl
-    from paper_2406_03243_amd.llmig import Pool
+    from paper_2406_03243_amd import migrate, scenarios
 
-    w = wl.LLAMA30B_TP4
-    shape = w.shape
-    log("allocating", w.name, shape)
-    sk, sv = harness.alloc_layers(shape)
-    dk, dv = harness.alloc_layers(shape)
-    harness.fill_on_device(sk + sv, w.seed * 16 + wl.SRC_VALUES)
-    harness.fill_on_device(dk + dv, w.seed * 16 + wl.DST_VALUES)
-    src, dst = Pool(sk, sv), Pool(dk, dv)
-    table, _ = wl.request_table(w.seed, shape.num_blocks, w.table_blocks)
-    free, _ = wl.free_list(w.seed, shape.num_blocks)
-    max_tok = 256
-    bits = wl.values16(w.seed, wl.APPEND_VALUES, shape.num_layers * 2 * max_tok * src.slot_bytes // 2, shape.dtype)
-    append_pool = torch.from_numpy(bits.view(np.uint8).reshape(shape.num_layers, 2, max_tok, src.slot_bytes)).cuda()
+    su = scenarios.llama30b_quarter()
+    shape, src, dst, table, free = su.shape, su.src, su.dst, su.tables[0], su.free
+    log("allocated", su.workload.name, shape)
+    append_pool = su.extra["append_pool"]
     mig, dec = torch.cuda.Stream(), torch.cuda.Stream()
-    out = {"workload": w.name, "layers": shape.num_layers, "kv_heads": shape.kv_heads,
+    out = {"workload": su.workload.name, "layers": shape.num_layers, "kv_heads": shape.kv_heads,
            "head_dim": shape.head_dim, "decode_step_ms": 20.0, "by_len": {}}
-    for length in w.lengths:
+    for length in su.lengths:
         log("downtime sweep", length)
         res = []
         for r in range(reps + 1):
@@ -298,8 +279,127 @@ def downtime_sweep(reps):
             "downtime_us_min": round(min(dt for _, dt in res), 1),
             "blocking_copy_downtime_us_median": round(statistics.median(blocking), 1),
         }
-    src.close()
-    dst.close()
+    su.close()
+    return out
+
+
+def batched_section(reps=10, host_reps=3, chunk_pairs=64):
+    """64 requests migrated in one llmig_stage call; and the same pairs
+    through pinned host memory (pack -> host -> unpack, chunked, two buffers)."""
+    import torch
+
+    from paper_2406_03243_amd import migrate, scenarios
+    from paper_2406_03243_amd.llmig import llmig_stage
+
+    su = scenarios.batched()
+    shape, src, dst = su.shape, su.src, su.dst
+    log("allocated", su.workload.name, shape)
+    ms, md, _ = migrate.plan_batch(su.tables, su.lengths, su.free, shape.block_size)
+    nbytes = stage_bytes(len(ms), shape, src.tile_bytes)
+    mig = torch.cuda.Stream()
+    for _ in range(3):
+        llmig_stage(src, dst, ms, md, stream=mig)
+    torch.cuda.synchronize()
+    times = []
+    for _ in range(reps):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(mig)
+        llmig_stage(src, dst, ms, md, stream=mig)
+        e1.record(mig)
+        torch.cuda.synchronize()
+        times.append(e0.elapsed_time(e1) * 1e3)
+    us = statistics.median(times)
+    out = {"workload": su.workload.name, "requests": len(su.tables), "pairs": int(len(ms)),
+           "pool_blocks": shape.num_blocks, "bytes": nbytes, "stage_us_median": round(us, 1),
+           "GBps": round(nbytes / (us * 1e-6) / 1e9, 1),
+           "lengths": {"min": int(min(su.lengths)), "median": float(statistics.median(su.lengths)),
+                       "max": int(max(su.lengths)), "tokens": int(sum(su.lengths))}}
+    chunk_bytes = chunk_pairs * shape.num_layers * 2 * src.tile_bytes
+    bufs = [torch.empty(chunk_bytes, dtype=torch.uint8, pin_memory=True) for _ in range(2)]
+    ps, us_ = torch.cuda.Stream(), torch.cuda.Stream()
+    host_times = []
+    for r in range(host_reps + 1):
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        migrate.run_host_staged(src, dst, ms, md, bufs, ps, us_, chunk_pairs)
+        torch.cuda.synchronize()
+        if r:
+            host_times.append(time.perf_counter() - t0)
+    ht = statistics.median(host_times)
+    one_way = len(ms) * shape.num_layers * 2 * src.tile_bytes
+    out["host_staged"] = {"chunk_pairs": chunk_pairs, "seconds_median": round(ht, 4),
+                          "bytes_each_way": one_way, "GBps_each_way": round(one_way / ht / 1e9, 2),
+                          "bound": "PCIe Gen5 x16, ~64 GB/s per direction"}
+    su.close()
+    return out
+
+
+def load_section(reps=3, reader_passes=3, step_ms=20.0):
+    """GQA long-context migration beside a streaming reader of a separate
+    40 GB region (all streams at the default priority)."""
+    import torch
+
+    from paper_2406_03243_amd import migrate, scenarios
+    from paper_2406_03243_amd.llmig import llmig_stream_read
+
+    su = scenarios.gqa_long()
+    shape, src, dst, table, free = su.shape, su.src, su.dst, su.tables[0], su.free
+    log("allocated", su.workload.name, shape)
+    region, append_pool = su.extra["region"], su.extra["append_pool"]
+    cus = torch.cuda.get_device_properties(0).multi_processor_count
+    wgs = cus * 4
+    sink = torch.empty(wgs * 256, dtype=torch.int64, device="cuda")
+    rd, mig, dec = torch.cuda.Stream(), torch.cuda.Stream(), torch.cuda.Stream()
+    length = su.lengths[0]
+
+    def reader_run():
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(rd)
+        llmig_stream_read(region, reader_passes, wgs, sink, stream=rd)
+        e1.record(rd)
+        return e0, e1
+
+    # alone: reader, then migration
+    alone_r, alone_m = [], []
+    for r in range(reps + 1):
+        e = reader_run()
+        torch.cuda.synchronize()
+        if r:
+            alone_r.append(e[0].elapsed_time(e[1]) * 1e3)
+    for r in range(reps + 1):
+        m, dt = migrate.run_timed(src, dst, table, length, free, append_pool, mig, dec, step_ms=step_ms)
+        if r:
+            alone_m.append((m, dt))
+    # together: the reader starts, then the migration
+    both = []
+    for r in range(reps + 1):
+        torch.cuda.synchronize()
+        e = reader_run()
+        t0 = time.perf_counter()
+        m, dt = migrate.run_timed(src, dst, table, length, free, append_pool, mig, dec, step_ms=step_ms)
+        t_mig = time.perf_counter() - t0
+        torch.cuda.synchronize()
+        if r:
+            both.append((e[0].elapsed_time(e[1]) * 1e3, m, dt, t_mig))
+    read_bytes = reader_passes * region.numel() * region.element_size()
+    r_alone = statistics.median(alone_r)
+    r_both = statistics.median(b[0] for b in both)
+    t_mig = statistics.median(b[3] for b in both) * 1e6
+    s1_bytes = stage_bytes(alone_m[0][0].stages[0].blocks, shape, src.tile_bytes)
+    s1_alone = statistics.median(m.stages[0].gpu_us for m, _ in alone_m)
+    s1_both = statistics.median(b[1].stages[0].gpu_us for b in both)
+    out = {"workload": su.workload.name, "tokens": length, "reader_bytes": read_bytes,
+           "reader_workgroups": wgs,
+           "reader_alone_GBps": round(read_bytes / (r_alone * 1e-6) / 1e9, 1),
+           "reader_with_migration_GBps": round(read_bytes / (r_both * 1e-6) / 1e9, 1),
+           "reader_slowdown_during_migration": round(max(0.0, r_both - r_alone) / t_mig, 3),
+           "migration_wall_us": round(t_mig, 1),
+           "stage1_GBps_alone": round(s1_bytes / (s1_alone * 1e-6) / 1e9, 1),
+           "stage1_GBps_under_load": round(s1_bytes / (s1_both * 1e-6) / 1e9, 1),
+           "stages_under_load": statistics.median(len(b[1].stages) for b in both),
+           "downtime_us_alone": round(statistics.median(dt for _, dt in alone_m), 1),
+           "downtime_us_under_load": round(statistics.median(b[2] for b in both), 1)}
+    su.close()
     return out
 
 

@@ -87,7 +87,8 @@ int64_t llmig_pool_tile_bytes(const llmig_pool *pool);
 
 /* Plans one migration stage (§4.2: before each stage the destination
  * pre-allocates the blocks the stage migrates).  Pure host function: no GPU
- * call, no allocation, reentrant.
+ * call, reentrant; it allocates host scratch only to check a stage of more
+ * than 32 blocks for repeated ids.
  *
  * The request has `len` tokens resident in the source pool; logical block j
  * holds tokens [j*block_size, (j+1)*block_size) and lives in source block
@@ -164,6 +165,17 @@ int llmig_unpack(const llmig_pool *dst, const int32_t *blocks, int64_t n, int ma
  * without a model. */
 int llmig_write_tokens(const llmig_pool *pool, const int32_t *table, int64_t table_len,
                        int64_t from_tok, int64_t n_tok, const void *data, void *stream);
+
+/* Stand-in for the decode work running beside a migration (its reads of
+ * the KV cache, §6.2 measures decode speed during migration): reads the
+ * `bytes` of device memory at `region` `passes` times with 16-byte loads on
+ * `workgroups` workgroups of 256 lanes, and stores what each lane read,
+ * summed as 32-bit integers, to out[lane] (so out must hold
+ * workgroups * 256 words).  Every
+ * lane runs exactly `passes` passes, so the work always completes.  region
+ * 16-byte aligned, bytes a positive multiple of 16 (else LLMIG_EINVAL). */
+int llmig_stream_read(const void *region, int64_t bytes, int32_t passes, int32_t workgroups,
+                      uint64_t *out, int64_t out_words, void *stream);
 
 /* Static description of a code; never NULL. */
 const char *llmig_strerror(int code);

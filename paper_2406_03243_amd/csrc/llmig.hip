@@ -222,6 +222,35 @@ __global__ void __launch_bounds__(kThreads) write_token_slots(const WriteArgs a)
     }
 }
 
+// Harness: a steady stream of HBM reads standing in for decode's KV reads.
+// Each lane sums (as 32-bit integers) the 16-byte words it reads and stores
+// its own result to out[global lane]; every lane runs a fixed number of
+// passes, so the grid always drains.
+__global__ void __launch_bounds__(kThreads) stream_read_words(const uint8_t *region, uint64_t words,
+                                                              uint32_t passes, uint64_t *out)
+{
+    constexpr int kLoads = 8;
+    const uint64_t lane = static_cast<uint64_t>(blockIdx.x) * kThreads + threadIdx.x;
+    const uint64_t lanes = static_cast<uint64_t>(gridDim.x) * kThreads;
+    u32x4 acc = {0u, 0u, 0u, 0u};
+    for (uint32_t p = 0; p < passes; ++p) {
+        uint64_t w = lane;
+        for (; w + (kLoads - 1) * lanes < words; w += kLoads * lanes) {
+            u32x4 r[kLoads];
+#pragma unroll
+            for (int u = 0; u < kLoads; ++u)
+                r[u] = load16(region + (w + u * lanes) * 16);
+#pragma unroll
+            for (int u = 0; u < kLoads; ++u)
+                acc += r[u];
+        }
+        for (; w < words; w += lanes)
+            acc += load16(region + w * 16);
+    }
+    const uint64_t folded = (static_cast<uint64_t>(acc.x + acc.z) << 32) | (acc.y + acc.w);
+    ((LLMIG_GLOBAL uint64_t *)out)[lane] = folded;
+}
+
 bool same_geometry(const llmig_pool *a, const llmig_pool *b)
 {
     return a->num_layers == b->num_layers && a->block_size == b->block_size &&
@@ -656,6 +685,22 @@ int llmig_write_tokens(const llmig_pool *pool, const int32_t *table, int64_t tab
         t = end;
     }
     return LLMIG_OK;
+}
+
+int llmig_stream_read(const void *region, int64_t bytes, int32_t passes, int32_t workgroups, uint64_t *out,
+                      int64_t out_words, void *stream)
+{
+    if (!region || !out || bytes <= 0 || bytes % 16 != 0 || passes <= 0 || workgroups <= 0 ||
+        (reinterpret_cast<uintptr_t>(region) & 15u) || (reinterpret_cast<uintptr_t>(out) & 7u) ||
+        out_words < static_cast<int64_t>(workgroups) * kThreads)
+        return LLMIG_EINVAL;
+    const uint8_t *r = static_cast<const uint8_t *>(region);
+    uint64_t words = static_cast<uint64_t>(bytes) / 16u;
+    uint32_t np = static_cast<uint32_t>(passes);
+    void *args[] = {&r, &words, &np, &out};
+    hipError_t e = hipLaunchKernel(reinterpret_cast<const void *>(&stream_read_words), dim3(workgroups),
+                                   dim3(kThreads), args, 0, static_cast<hipStream_t>(stream));
+    return e == hipSuccess ? LLMIG_OK : hip_error(e);
 }
 
 const char *llmig_strerror(int code)

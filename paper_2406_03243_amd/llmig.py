@@ -64,6 +64,8 @@ _lib.llmig_unpack.argtypes = [_vp, _vp, ctypes.c_int64, ctypes.c_int, _vp, ctype
 _lib.llmig_unpack.restype = ctypes.c_int
 _lib.llmig_write_tokens.argtypes = [_vp, _vp, ctypes.c_int64, ctypes.c_int64, ctypes.c_int64, _vp, _vp]
 _lib.llmig_write_tokens.restype = ctypes.c_int
+_lib.llmig_stream_read.argtypes = [_vp, ctypes.c_int64, ctypes.c_int32, ctypes.c_int32, _vp, ctypes.c_int64, _vp]
+_lib.llmig_stream_read.restype = ctypes.c_int
 _lib.llmig_strerror.argtypes = [ctypes.c_int]
 _lib.llmig_strerror.restype = ctypes.c_char_p
 _lib.llmig_last_hip_error.argtypes = []
@@ -215,5 +217,11 @@ def llmig_write_tokens(pool: Pool, table, from_tok: int, data: torch.Tensor, str
                                    data.data_ptr(), _stream(stream)), "llmig_write_tokens")
 
 
-def exported_symbols():
-    return _lib
+def llmig_stream_read(region: torch.Tensor, passes: int, workgroups: int, out: torch.Tensor, stream=None) -> None:
+    """Harness: read ``region`` ``passes`` times on ``workgroups`` workgroups
+    (decode stand-in); ``out`` is a CUDA int64 tensor of workgroups * 256."""
+    if not region.is_cuda or not out.is_cuda or out.dtype != torch.int64:
+        raise ValueError("region and out must be CUDA tensors, out int64")
+    _check(_lib.llmig_stream_read(region.data_ptr(), region.numel() * region.element_size(), int(passes),
+                                  int(workgroups), out.data_ptr(), out.numel(), _stream(stream)),
+           "llmig_stream_read")

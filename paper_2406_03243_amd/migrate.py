@@ -23,7 +23,7 @@ from dataclasses import dataclass, field
 import numpy as np
 import torch
 
-from .llmig import Pool, llmig_plan, llmig_stage, llmig_write_tokens
+from .llmig import Pool, llmig_pack, llmig_plan, llmig_stage, llmig_unpack, llmig_write_tokens
 
 
 @dataclass
@@ -89,13 +89,6 @@ class Migration:
                 rec.gpu_us = ev[0].elapsed_time(ev[1]) * 1e3
 
 
-def wait_spin(stream) -> None:
-    """Wait for a stream by polling it: on the downtime path this returns
-    sooner after the copy ends than a blocking wait, which may sleep."""
-    while not stream.query():
-        pass
-
-
 def run_scheduled(src: Pool, dst: Pool, src_table, dst_free_list, initial_len: int, appends,
                   mig_stream, dec_stream, time_all: bool = False):
     """A migration whose decoding appends a known batch of tokens before each
@@ -126,7 +119,7 @@ def run_scheduled(src: Pool, dst: Pool, src_table, dst_free_list, initial_len: i
             ev.synchronize()
             t0 = time.perf_counter()
             m.stage(length, final=True, time_it=False)
-            wait_spin(mig_stream)
+            mig_stream.synchronize()
             downtime_us = (time.perf_counter() - t0) * 1e6
         else:
             mig_stream.wait_event(ev)
@@ -173,10 +166,50 @@ def run_timed(src: Pool, dst: Pool, src_table, initial_len: int, dst_free_list, 
             ev.synchronize()
             t0 = time.perf_counter()
             m.stage(length, final=True, time_it=False)
-            wait_spin(mig_stream)
+            mig_stream.synchronize()
             downtime_us = (time.perf_counter() - t0) * 1e6
             break
         mig_stream.wait_event(ev)
         rec = m.stage(length, final=False)
     m.collect_times()
     return m, downtime_us
+
+
+def plan_batch(tables, lengths, dst_free_list, block_size: int):
+    """Plan a batched migration of several requests as one stage each
+    (request order, destination blocks taken from the head of the free list
+    in turn).  Returns (map_src, map_dst, per-request destination tables)."""
+    free = np.ascontiguousarray(np.asarray(dst_free_list, dtype=np.int32))
+    srcs, dsts = [], []
+    for table, length in zip(tables, lengths):
+        ms, md = llmig_plan(table, free, int(length), 0, int(length), block_size)
+        srcs.append(ms)
+        dsts.append(md)
+        free = free[len(md):]
+    return np.concatenate(srcs), np.concatenate(dsts), dsts
+
+
+def run_host_staged(src: Pool, dst: Pool, map_src, map_dst, host_bufs, pack_stream, unpack_stream,
+                    chunk_pairs: int):
+    """Block fusion through pinned host memory (Llumnix §5): chunks of
+    ``chunk_pairs`` block pairs are packed from the source pool into one of
+    two pinned host buffers (the kernel stores over PCIe) and unpacked from
+    it into the destination pool (the kernel loads over PCIe), the two
+    buffers alternating so that packing chunk k+1 overlaps unpacking chunk k.
+    Events order each unpack after its pack and each reuse of a buffer after
+    the unpack that read it.  Returns once all work is enqueued."""
+    n = len(map_src)
+    unpacked = [None, None]
+    for c, lo in enumerate(range(0, n, chunk_pairs)):
+        hi = min(n, lo + chunk_pairs)
+        buf = host_bufs[c % 2]
+        if unpacked[c % 2] is not None:
+            pack_stream.wait_event(unpacked[c % 2])
+        llmig_pack(src, map_src[lo:hi], buf, stream=pack_stream)
+        packed = torch.cuda.Event()
+        packed.record(pack_stream)
+        unpack_stream.wait_event(packed)
+        llmig_unpack(dst, map_dst[lo:hi], buf, stream=unpack_stream)
+        ev = torch.cuda.Event()
+        ev.record(unpack_stream)
+        unpacked[c % 2] = ev

@@ -110,6 +110,24 @@ def request_table(seed: int, num_blocks: int, count: int, preoccupied: float = 0
     return table, occupied
 
 
+def request_tables(seed: int, num_blocks: int, counts, preoccupied: float = 0.0):
+    """Block tables of several requests sharing one pool: request k gets
+    counts[k] distinct blocks, no block shared between requests or with the
+    blocks other requests hold; every table is in random order.  Returns
+    (tables, occupied_by_others)."""
+    occupied, free = pool_layout(seed, SRC_LAYOUT, num_blocks, preoccupied)
+    need = int(sum(counts))
+    if need > len(free):
+        raise ValueError("pool too small for the requests")
+    g = stream(seed, SRC_LAYOUT, 1)
+    pick = g.permutation(free)[:need].astype(np.int32)
+    tables, at = [], 0
+    for c in counts:
+        tables.append(pick[at:at + int(c)].copy())
+        at += int(c)
+    return tables, occupied
+
+
 def free_list(seed: int, num_blocks: int, preoccupied: float = 0.0):
     """The destination's free list: its free blocks in random order.
     Returns (free_list, occupied_by_others)."""

@@ -1,0 +1,215 @@
+"""Parity at the full workload sizes, through the same set-up
+(paper_2406_03243_amd.scenarios) and drivers the benchmark times.
+
+Pools here are tens of GB, so the oracle runs on compact host pools: the
+blocks a migration touches, snapshotted before it starts, behind an id remap
+(request block j -> compact id j, consumed destination block k -> compact id
+k).  Where even that is too large, a sample of pairs is replayed by the oracle
+and every pair is checked on the device for equality of source and
+destination tiles (a property that holds at any size).  Tolerance 0."""
+import sys
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from oracle import HostPool
+from paper_2406_03243_amd import harness
+from paper_2406_03243_amd import workloads as wl
+
+pytestmark = pytest.mark.gpu
+
+if torch.cuda.is_available():
+    from paper_2406_03243_amd import migrate, scenarios
+    from paper_2406_03243_amd.llmig import llmig_stage, llmig_stream_read
+
+
+def say(*a):
+    print("[case]", *a, flush=True)
+    sys.stdout.flush()
+
+
+@pytest.fixture(autouse=True)
+def release_memory():
+    yield
+    torch.cuda.synchronize()
+    torch.cuda.empty_cache()
+
+
+def compact(pool, ids) -> HostPool:
+    return HostPool(harness.snapshot_blocks(pool.k, ids), harness.snapshot_blocks(pool.v, ids),
+                    pool.block_size, pool.slot_bytes)
+
+
+def assert_same(a: HostPool, b: HostPool, what: str):
+    for l in range(b.num_layers):
+        for kv, (x, y) in enumerate(((a.k[l], b.k[l]), (a.v[l], b.v[l]))):
+            if not np.array_equal(x, y):
+                bad = np.nonzero((x != y).any(axis=1))[0]
+                raise AssertionError(f"{what}: layer {l} {'KV'[kv]} differs in compact blocks "
+                                     f"{bad[:10].tolist()} ({len(bad)})")
+
+
+def device_pairs_equal(src, dst, ms, md) -> bool:
+    """Every destination tile equals its source tile, checked on the GPU."""
+    si = torch.as_tensor(np.asarray(ms, np.int64), device="cuda")
+    di = torch.as_tensor(np.asarray(md, np.int64), device="cuda")
+    for a, b in zip(src.k + src.v, dst.k + dst.v):
+        if not torch.equal(harness.tile_view(a).index_select(0, si), harness.tile_view(b).index_select(0, di)):
+            return False
+    return True
+
+
+def untouched_sample(dst, mapped, k, seed):
+    rest = np.setdiff1d(np.arange(dst.num_blocks), mapped)
+    return np.sort(wl.stream(seed, wl.EXTRA, 7).choice(rest, min(k, len(rest)), replace=False)).astype(np.int32)
+
+
+def test_llama7b_multistage_full():
+    """The benchmark's workload, every mapped block replayed by the oracle."""
+    su = scenarios.llama7b()
+    say("llama7b full", su.shape, su.counts)
+    table, free = su.tables[0], su.free
+    total = su.lengths[0] + sum(su.counts)
+    nb = -(-total // su.shape.block_size)
+    used = free[:nb]
+    hs = compact(su.src, table[:nb])
+    hd = compact(su.dst, used)
+    guard = untouched_sample(su.dst, used, 256, 1)
+    guard_before = compact(su.dst, guard)
+    host_appends = [a.cpu().numpy().reshape(su.shape.num_layers, 2, c, su.src.slot_bytes)
+                    for a, c in zip(su.appends, su.counts)]
+    mig, dec = torch.cuda.Stream(), torch.cuda.Stream()
+    m, downtime = migrate.run_scheduled(su.src, su.dst, table, free, su.lengths[0], su.appends, mig, dec)
+    torch.cuda.synchronize()
+    assert len(m.stages) == 5 and m.stages[-1].final
+    assert np.array_equal(m.dst_table, used)
+    # oracle replay on compact pools: logical block j -> compact j, destination k -> compact k
+    events, cur = [], su.lengths[0]
+    bounds = oracle.stage_bounds(su.lengths[0], su.counts, su.shape.block_size)
+    for k, (length, lo, hi) in enumerate(bounds):
+        if k:
+            events.append(("append", cur, host_appends[k - 1]))
+            cur += su.counts[k - 1]
+        events.append(("stage", length, lo, hi))
+    assert [(r.length, r.from_tok, r.to_tok) for r in m.stages] == bounds
+    ctable = np.arange(nb, dtype=np.int32)
+    dst_table, _ = oracle.default().migrate(hs, hd, ctable, np.arange(nb, dtype=np.int32), events)
+    assert np.array_equal(dst_table, ctable)
+    assert_same(compact(su.dst, used), hd, "destination blocks")
+    assert_same(compact(su.src, table[:nb]), hs, "source blocks (with appends)")
+    assert oracle.default().first_token_mismatch(hs, ctable, compact(su.dst, used), ctable, total) == -1
+    assert_same(compact(su.dst, guard), guard_before, "destination blocks outside the mapping")
+    su.close()
+
+
+def test_llama30b_quarter_full_16k():
+    su = scenarios.llama30b_quarter()
+    length = 16384
+    say("llama30b quarter full", su.shape, length)
+    table, free = su.tables[0], su.free
+    cap = 1040
+    hs = compact(su.src, table[:cap])
+    hd = compact(su.dst, free[:cap])
+    mig, dec = torch.cuda.Stream(), torch.cuda.Stream()
+    pool = su.extra["append_pool"]
+    m, downtime = migrate.run_timed(su.src, su.dst, table, length, free, pool, mig, dec, step_ms=20.0)
+    torch.cuda.synchronize()
+    assert m.stages[-1].final and m.stages[-1].blocks <= 1
+    host_pool = pool.cpu().numpy()
+    events, cur, used_tok = [], length, 0
+    for r in m.stages:
+        if r.length > cur:
+            n = r.length - cur
+            events.append(("append", cur, np.ascontiguousarray(host_pool[:, :, used_tok:used_tok + n])))
+            used_tok += n
+            cur = r.length
+        events.append(("stage", r.length, r.from_tok, r.to_tok))
+    nb = len(m.dst_table)
+    assert nb == -(-cur // su.shape.block_size)
+    ctab = np.arange(cap, dtype=np.int32)
+    dst_table, _ = oracle.default().migrate(hs, hd, ctab, ctab, events)
+    assert np.array_equal(dst_table, ctab[:nb])
+    assert_same(compact(su.dst, free[:cap]), hd, "destination blocks")
+    assert oracle.default().first_token_mismatch(hs, ctab, hd, ctab, cur) == -1
+    su.close()
+
+
+def test_batched_one_call_full():
+    su = scenarios.batched()
+    say("batched full", su.shape, len(su.tables))
+    ms, md, per_req = migrate.plan_batch(su.tables, su.lengths, su.free, su.shape.block_size)
+    assert len(ms) == sum(-(-n // su.shape.block_size) for n in su.lengths)
+    sample = np.sort(wl.stream(su.workload.seed, wl.EXTRA, 3).choice(len(ms), 256, replace=False))
+    hs = compact(su.src, ms[sample])
+    hd = compact(su.dst, md[sample])
+    guard = untouched_sample(su.dst, md, 256, 2)
+    guard_before = compact(su.dst, guard)
+    src_occ = su.src_occupied[:256]
+    src_occ_before = compact(su.src, src_occ)
+    llmig_stage(su.src, su.dst, ms, md)
+    torch.cuda.synchronize()
+    ids = np.arange(len(sample), dtype=np.int32)
+    oracle.default().copy(hs, hd, ids, ids)
+    assert_same(compact(su.dst, md[sample]), hd, "sampled destination blocks")
+    assert device_pairs_equal(su.src, su.dst, ms, md)
+    assert_same(compact(su.dst, guard), guard_before, "destination blocks outside the mapping")
+    assert_same(compact(su.src, src_occ), src_occ_before, "source blocks of other requests")
+    su.close()
+
+
+def test_batched_host_staged_full():
+    su = scenarios.batched()
+    say("batched host staged", su.shape)
+    ms, md, _ = migrate.plan_batch(su.tables, su.lengths, su.free, su.shape.block_size)
+    sample = np.sort(wl.stream(su.workload.seed, wl.EXTRA, 4).choice(len(ms), 128, replace=False))
+    hs = compact(su.src, ms[sample])
+    hd = compact(su.dst, md[sample])
+    guard = untouched_sample(su.dst, md, 128, 3)
+    guard_before = compact(su.dst, guard)
+    chunk = 64
+    nbytes = chunk * su.shape.num_layers * 2 * su.src.tile_bytes
+    bufs = [torch.empty(nbytes, dtype=torch.uint8, pin_memory=True) for _ in range(2)]
+    migrate.run_host_staged(su.src, su.dst, ms, md, bufs, torch.cuda.Stream(), torch.cuda.Stream(), chunk)
+    torch.cuda.synchronize()
+    ids = np.arange(len(sample), dtype=np.int32)
+    oracle.default().copy(hs, hd, ids, ids)
+    assert_same(compact(su.dst, md[sample]), hd, "sampled destination blocks")
+    assert device_pairs_equal(su.src, su.dst, ms, md)
+    assert_same(compact(su.dst, guard), guard_before, "destination blocks outside the mapping")
+    su.close()
+
+
+def test_gqa_long_under_load():
+    su = scenarios.gqa_long()
+    say("gqa long under load", su.shape)
+    table, free = su.tables[0], su.free
+    length = su.lengths[0]
+    cap = su.workload.table_blocks
+    pool = su.extra["append_pool"]
+    hs = compact(su.src, table[:cap])
+    hd = compact(su.dst, free[:cap])
+    region = su.extra["region"]
+    wgs = torch.cuda.get_device_properties(0).multi_processor_count * 4
+    sink = torch.empty(wgs * 256, dtype=torch.int64, device="cuda")
+    rd, mig, dec = torch.cuda.Stream(), torch.cuda.Stream(), torch.cuda.Stream()
+    llmig_stream_read(region, 2, wgs, sink, stream=rd)
+    m, downtime = migrate.run_timed(su.src, su.dst, table, length, free, pool, mig, dec, step_ms=20.0)
+    torch.cuda.synchronize()
+    host_pool = pool.cpu().numpy()
+    events, cur, used_tok = [], length, 0
+    for r in m.stages:
+        if r.length > cur:
+            n = r.length - cur
+            events.append(("append", cur, np.ascontiguousarray(host_pool[:, :, used_tok:used_tok + n])))
+            used_tok += n
+            cur = r.length
+        events.append(("stage", r.length, r.from_tok, r.to_tok))
+    ctab = np.arange(cap, dtype=np.int32)
+    dst_table, _ = oracle.default().migrate(hs, hd, ctab, ctab, events)
+    assert_same(compact(su.dst, free[:cap]), hd, "destination blocks")
+    assert oracle.default().first_token_mismatch(hs, ctab, hd, ctab, cur) == -1
+    # the reader really read: its sums are not all zero
+    assert bool((sink != 0).any())
+    su.close()
