@@ -20,6 +20,7 @@ tensor-parallel-quarter shape (60 layers, 13 heads of 128; 1k/4k/16k tokens).
 from __future__ import annotations
 
 import argparse
+import gc
 import json
 import math
 import os
@@ -69,6 +70,7 @@ def main():
     ap.add_argument("--sections", default="downtime,batched,load",
                     help="extra workloads after the main one (comma list of downtime, batched, load; empty for none)")
     ap.add_argument("--downtime-reps", type=int, default=7)
+    ap.add_argument("--no-gc-freeze", action="store_true", help="leave set-up objects to the collector")
     ap.add_argument("--calibration-copy", action="store_true",
                     help="end with two plain 1 GiB device-to-device copies (hardware counter calibration)")
     args = ap.parse_args()
@@ -101,19 +103,34 @@ def main():
     def step():
         return migrate.run_scheduled(src, dst, table, free, initial, appends, mig, dec)
 
+    # Long-lived objects (torch, the pools) go to the permanent generation, so
+    # that a full collection during the timed steps does not walk them.
+    gc.collect()
+    if not args.no_gc_freeze:
+        gc.freeze()
+    collections = {0: 0, 1: 0, 2: 0}
+
+    def on_gc(phase, info):
+        if phase == "start":
+            collections[info["generation"]] += 1
+
     log(f"warmup {args.warmup}")
     for _ in range(args.warmup):
         step()
     torch.cuda.synchronize()
 
     log(f"timing {args.steps} steps")
-    runs = []
+    runs, marks = [], []
     torch.cuda.synchronize()
+    gc.callbacks.append(on_gc)
     t0 = time.perf_counter()
     for _ in range(args.steps):
-        runs.append(step())
+        runs.append(step())          # each step ends on its final stage's synchronisation
+        marks.append(time.perf_counter())
     torch.cuda.synchronize()
     elapsed = time.perf_counter() - t0
+    gc.callbacks.remove(on_gc)
+    step_ms = [(b - a) * 1e3 for a, b in zip([t0] + marks[:-1], marks)]
 
     m0 = runs[0][0]
     blocks_per_step = sum(r.blocks for r in m0.stages)
@@ -151,6 +168,9 @@ def main():
         "steps": args.steps,
         "warmup": args.warmup,
         "ms_per_step": round(ms_per_step, 4),
+        "step_ms": {"median": round(statistics.median(step_ms), 4), "min": round(min(step_ms), 4),
+                    "max": round(max(step_ms), 4), "all": [round(x, 3) for x in step_ms],
+                    "gc_collections": {f"gen{g}": n for g, n in collections.items()}},
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
@@ -175,7 +195,7 @@ def main():
 
     # ------------------------------------------------------------------ CPU oracle baseline
     if not args.no_cpu_baseline:
-        result["cpu_baseline"] = cpu_baseline(src, m0.stages[0], shape, args.cpu_seconds)
+        result["cpu_baseline"] = cpu_baseline(src, table, free, m0.stages[0], shape, args.cpu_seconds)
 
     if args.calibration_copy:
         a = torch.empty(1 << 30, dtype=torch.uint8, device=dev)
@@ -205,7 +225,7 @@ def main():
     print(json.dumps(result), flush=True)
 
 
-def cpu_baseline(src, stage1, shape, seconds):
+def cpu_baseline(src, table, free, stage1, shape, seconds):
     """The oracle's per-tile copy on host snapshots of a sample of stage 1's
     blocks, single-threaded, repeated for about ``seconds``."""
     import numpy as np
@@ -214,8 +234,11 @@ def cpu_baseline(src, stage1, shape, seconds):
     from oracle import HostPool
     from paper_2406_03243_amd import harness
 
+    from paper_2406_03243_amd.llmig import llmig_plan
+
     n = 64
-    ms, md = stage1.map_src[:n], stage1.map_dst[:n]
+    ms, md = llmig_plan(table, free, stage1.length, stage1.from_tok, stage1.to_tok, src.block_size)
+    ms, md = ms[:n], md[:n]
     hs = HostPool(harness.snapshot_blocks(src.k, ms), harness.snapshot_blocks(src.v, ms),
                   src.block_size, src.slot_bytes)
     hd = HostPool.zeros(shape.num_layers, n, src.block_size, src.slot_bytes)

@@ -166,6 +166,81 @@ int llmig_unpack(const llmig_pool *dst, const int32_t *blocks, int64_t n, int ma
 int llmig_write_tokens(const llmig_pool *pool, const int32_t *table, int64_t table_len,
                        int64_t from_tok, int64_t n_tok, const void *data, void *stream);
 
+/* ---------------------------------------------------------------------------
+ * Migration coordinator: the handshake of §4.2 as a host state machine.
+ *
+ * Before each stage the source asks the destination to pre-allocate the
+ * blocks the stage migrates; the destination reserves them or refuses, and a
+ * refusal aborts the migration.  After each stage the source checks whether
+ * the request finished or was preempted, and aborts (releasing the reserved
+ * blocks) if so; either side aborts when the other fails.  After the final
+ * stage the source releases its blocks and the destination commits.
+ *
+ * A llmig_migration holds the request's progress: tokens copied so far, the
+ * destination blocks reserved so far (in logical order), the stage count and
+ * its state.  It owns no pool memory and no free list: the caller passes the
+ * destination's current free list to each stage and drops the consumed
+ * entries from its head.  Stages are planned exactly as llmig_plan plans them
+ * (whole blocks only in a non-final stage).  A migration is not thread-safe;
+ * use one per request.
+ * ------------------------------------------------------------------------- */
+
+#define LLMIG_MIGRATION_ACTIVE 0    /* stages may follow */
+#define LLMIG_MIGRATION_FINISHED 1  /* the final stage ran; commit or abort */
+#define LLMIG_MIGRATION_COMMITTED 2
+#define LLMIG_MIGRATION_ABORTED 3
+
+typedef struct llmig_migration llmig_migration;
+
+/* Starts a migration for pools of the given block size.  Host only; no GPU
+ * call.  LLMIG_EINVAL for block_size < 1 or out == NULL. */
+int llmig_migration_create(int32_t block_size, llmig_migration **out);
+
+/* Frees the object.  It does not wait for enqueued copies.  NULL allowed. */
+void llmig_migration_destroy(llmig_migration *m);
+
+/* Pre-allocates and plans the next stage without copying (host only).  The
+ * request now holds `len` tokens whose blocks are src_table[0..]; a
+ * non-final stage covers [copied, floor(len/bs)*bs), the final one
+ * [copied, len).  Its pairs go to out_src/out_dst (capacity out_cap), *out_n
+ * is their count and the number of free-list entries consumed, and the
+ * destination ids join the migration's reservation.  Errors leave the
+ * migration unchanged: LLMIG_EINVAL (not ACTIVE, len below the tokens already
+ * copied, or any llmig_plan argument error), LLMIG_ENOSPC (the destination
+ * cannot reserve the stage: the caller should abort), LLMIG_ERANGE. */
+int llmig_migration_next(llmig_migration *m, const int32_t *src_table, int64_t src_table_len,
+                         int64_t len, int final_stage, const int32_t *dst_free_list, int64_t dst_free_len,
+                         int32_t *out_src, int32_t *out_dst, int64_t out_cap, int64_t *out_n);
+
+/* llmig_migration_next followed by llmig_stage of its pairs on `stream`, in
+ * one call (the ids travel in the kernel arguments).  *out_n is the number
+ * of free-list entries consumed.  src and dst are checked as llmig_stage
+ * checks them, and ids against the pools, before anything is reserved.  On
+ * LLMIG_EHIP the stage's blocks stay reserved (abort returns them) and part
+ * of the copy may have been enqueued. */
+int llmig_migration_stage(llmig_migration *m, const llmig_pool *src, const llmig_pool *dst,
+                          const int32_t *src_table, int64_t src_table_len, int64_t len, int final_stage,
+                          const int32_t *dst_free_list, int64_t dst_free_len, void *stream, int64_t *out_n);
+
+/* Aborts (ACTIVE or FINISHED): writes every reserved destination block to
+ * out (capacity cap; *out_n = count) so the destination can release them,
+ * and moves to ABORTED.  Copies already enqueued may still write into those
+ * blocks: synchronise the migration stream before reusing them.
+ * LLMIG_EINVAL if already COMMITTED or ABORTED, or cap is too small (then
+ * nothing changes). */
+int llmig_migration_abort(llmig_migration *m, int32_t *out, int64_t cap, int64_t *out_n);
+
+/* Commits (FINISHED only): writes the request's destination block table
+ * (one id per logical block, ceil(len/bs) of them) to out and moves to
+ * COMMITTED; the source may now release its blocks.  LLMIG_EINVAL when the
+ * final stage has not run, or cap is too small (then nothing changes). */
+int llmig_migration_commit(llmig_migration *m, int32_t *out, int64_t cap, int64_t *out_n);
+
+/* Progress: state (LLMIG_MIGRATION_*), tokens copied, blocks reserved,
+ * stages run.  Any output pointer may be NULL.  LLMIG_EINVAL for m == NULL. */
+int llmig_migration_info(const llmig_migration *m, int32_t *state, int64_t *copied_tokens,
+                         int64_t *reserved_blocks, int64_t *stages);
+
 /* Stand-in for the decode work running beside a migration (its reads of
  * the KV cache, §6.2 measures decode speed during migration): reads the
  * `bytes` of device memory at `region` `passes` times with 16-byte loads on

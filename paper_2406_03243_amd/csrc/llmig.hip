@@ -48,6 +48,16 @@ struct llmig_pool {
     std::vector<std::pair<uint64_t, uint64_t>> spans; // sorted [begin, end) of every layer tensor
 };
 
+struct llmig_migration {
+    int32_t block_size;
+    int32_t state;
+    int64_t copied_tok;               // tokens copied by the stages so far
+    int64_t stages;
+    std::vector<int32_t> reserved;    // destination blocks, in logical order
+    std::vector<int32_t> plan_src;    // per-stage scratch, reused
+    std::vector<int32_t> plan_dst;
+};
+
 namespace {
 
 constexpr int kThreads = 256;                 // 4 wavefronts of 64 lanes
@@ -458,6 +468,48 @@ int fused_copy_checks(const llmig_pool *pool, const int32_t *blocks, int64_t n, 
     return LLMIG_OK;
 }
 
+bool pools_compatible(const llmig_pool *src, const llmig_pool *dst)
+{
+    return same_geometry(src, dst) && src->device == dst->device && !pools_overlap(src, dst);
+}
+
+int check_pair_ids(const llmig_pool *src, const llmig_pool *dst, const int32_t *ms, const int32_t *md, int64_t n)
+{
+    int rc = check_ids(ms, n, src->num_blocks);
+    return rc == LLMIG_OK ? check_ids(md, n, dst->num_blocks) : rc;
+}
+
+int launch_stage(const llmig_pool *src, const llmig_pool *dst, const int32_t *ms, const int32_t *md, int64_t n,
+                 bool ids_on_device, hipStream_t stream)
+{
+    CopyArgs a;
+    std::memset(&a, 0, sizeof(a));
+    a.src_tab = src->d_tab;
+    a.dst_tab = dst->d_tab;
+    a.tile_bytes = static_cast<uint32_t>(src->tile_bytes);
+    a.num_layers = static_cast<uint32_t>(src->num_layers);
+    return launch_copy<kPool, kPool>(a, ms, md, n, ids_on_device, stream);
+}
+
+// Token range of the next stage of m for a request now holding len tokens.
+int next_range(const llmig_migration *m, int64_t len, int final_stage, int64_t *from, int64_t *to)
+{
+    if (m->state != LLMIG_MIGRATION_ACTIVE || len < m->copied_tok || (final_stage != 0 && final_stage != 1))
+        return LLMIG_EINVAL;
+    *from = m->copied_tok;
+    *to = final_stage ? len : (len / m->block_size) * m->block_size;
+    return LLMIG_OK;
+}
+
+void record_stage(llmig_migration *m, const int32_t *dst_ids, int64_t n, int64_t to, int final_stage)
+{
+    m->reserved.insert(m->reserved.end(), dst_ids, dst_ids + n); // n <= free list: memory the caller holds
+    m->copied_tok = to;
+    m->stages += 1;
+    if (final_stage)
+        m->state = LLMIG_MIGRATION_FINISHED;
+}
+
 } // namespace
 
 extern "C" {
@@ -573,29 +625,159 @@ int llmig_stage(const llmig_pool *src, const llmig_pool *dst, const int32_t *map
 {
     if (!src || !dst || n < 0 || (map_on_device != 0 && map_on_device != 1))
         return LLMIG_EINVAL;
-    if (!same_geometry(src, dst) || src->device != dst->device || pools_overlap(src, dst))
+    if (!pools_compatible(src, dst))
         return LLMIG_EINVAL;
     if (n == 0)
         return LLMIG_OK;
     if (!map_src || !map_dst)
         return LLMIG_EINVAL;
     if (!map_on_device) {
-        int rc = check_ids(map_src, n, src->num_blocks);
-        if (rc == LLMIG_OK)
-            rc = check_ids(map_dst, n, dst->num_blocks);
+        int rc = check_pair_ids(src, dst, map_src, map_dst, n);
         if (rc != LLMIG_OK)
             return rc;
         if (has_repeat(map_dst, n, dst->num_blocks))
             return LLMIG_EINVAL;
     }
-    CopyArgs a;
-    std::memset(&a, 0, sizeof(a));
-    a.src_tab = src->d_tab;
-    a.dst_tab = dst->d_tab;
-    a.tile_bytes = static_cast<uint32_t>(src->tile_bytes);
-    a.num_layers = static_cast<uint32_t>(src->num_layers);
-    return launch_copy<kPool, kPool>(a, map_src, map_dst, n, map_on_device != 0,
-                                     static_cast<hipStream_t>(stream));
+    return launch_stage(src, dst, map_src, map_dst, n, map_on_device != 0, static_cast<hipStream_t>(stream));
+}
+
+int llmig_migration_create(int32_t block_size, llmig_migration **out)
+{
+    if (!out)
+        return LLMIG_EINVAL;
+    *out = nullptr;
+    if (block_size < 1)
+        return LLMIG_EINVAL;
+    llmig_migration *m = new (std::nothrow) llmig_migration();
+    if (!m)
+        return LLMIG_EINVAL;
+    m->block_size = block_size;
+    m->state = LLMIG_MIGRATION_ACTIVE;
+    m->copied_tok = 0;
+    m->stages = 0;
+    *out = m;
+    return LLMIG_OK;
+}
+
+void llmig_migration_destroy(llmig_migration *m)
+{
+    delete m;
+}
+
+int llmig_migration_next(llmig_migration *m, const int32_t *src_table, int64_t src_table_len, int64_t len,
+                         int final_stage, const int32_t *dst_free_list, int64_t dst_free_len, int32_t *out_src,
+                         int32_t *out_dst, int64_t out_cap, int64_t *out_n)
+{
+    if (!m || !out_n)
+        return LLMIG_EINVAL;
+    *out_n = 0;
+    int64_t from = 0, to = 0;
+    int rc = next_range(m, len, final_stage, &from, &to);
+    if (rc != LLMIG_OK)
+        return rc;
+    int64_t n = 0;
+    rc = llmig_plan(src_table, src_table_len, dst_free_list, dst_free_len, len, from, to, m->block_size, out_src,
+                    out_dst, out_cap, &n);
+    if (rc != LLMIG_OK)
+        return rc;
+    record_stage(m, out_dst, n, to, final_stage);
+    *out_n = n;
+    return LLMIG_OK;
+}
+
+int llmig_migration_stage(llmig_migration *m, const llmig_pool *src, const llmig_pool *dst,
+                          const int32_t *src_table, int64_t src_table_len, int64_t len, int final_stage,
+                          const int32_t *dst_free_list, int64_t dst_free_len, void *stream, int64_t *out_n)
+{
+    if (!m || !out_n)
+        return LLMIG_EINVAL;
+    *out_n = 0;
+    if (!src || !dst || !pools_compatible(src, dst) || src->block_size != m->block_size)
+        return LLMIG_EINVAL;
+    int64_t from = 0, to = 0;
+    int rc = next_range(m, len, final_stage, &from, &to);
+    if (rc != LLMIG_OK)
+        return rc;
+    // Scratch for the stage's pairs: never more than the free list can give
+    // (a longer stage fails in llmig_plan before anything is written).
+    const int64_t bs = m->block_size;
+    const int64_t need = to / bs + (to % bs != 0) - from / bs;
+    if (need < 0 || dst_free_len < 0)
+        return LLMIG_EINVAL;
+    const size_t cap = static_cast<size_t>(std::max<int64_t>(std::min(need, dst_free_len), 1));
+    if (m->plan_src.size() < cap) {
+        try {
+            m->plan_src.resize(cap);
+            m->plan_dst.resize(cap);
+        } catch (...) {
+            return LLMIG_EINVAL;
+        }
+    }
+    int64_t n = 0;
+    rc = llmig_plan(src_table, src_table_len, dst_free_list, dst_free_len, len, from, to, m->block_size,
+                    m->plan_src.data(), m->plan_dst.data(), static_cast<int64_t>(cap), &n);
+    if (rc != LLMIG_OK)
+        return rc;
+    rc = check_pair_ids(src, dst, m->plan_src.data(), m->plan_dst.data(), n);
+    if (rc != LLMIG_OK)
+        return rc;
+    record_stage(m, m->plan_dst.data(), n, to, final_stage);
+    *out_n = n;
+    if (n == 0)
+        return LLMIG_OK;
+    return launch_stage(src, dst, m->plan_src.data(), m->plan_dst.data(), n, false,
+                        static_cast<hipStream_t>(stream));
+}
+
+int llmig_migration_abort(llmig_migration *m, int32_t *out, int64_t cap, int64_t *out_n)
+{
+    if (!m || !out_n)
+        return LLMIG_EINVAL;
+    *out_n = 0;
+    if (m->state != LLMIG_MIGRATION_ACTIVE && m->state != LLMIG_MIGRATION_FINISHED)
+        return LLMIG_EINVAL;
+    const int64_t n = static_cast<int64_t>(m->reserved.size());
+    if (cap < n || (n > 0 && !out))
+        return LLMIG_EINVAL;
+    if (n > 0)
+        std::memcpy(out, m->reserved.data(), static_cast<size_t>(n) * sizeof(int32_t));
+    m->reserved.clear();
+    m->state = LLMIG_MIGRATION_ABORTED;
+    *out_n = n;
+    return LLMIG_OK;
+}
+
+int llmig_migration_commit(llmig_migration *m, int32_t *out, int64_t cap, int64_t *out_n)
+{
+    if (!m || !out_n)
+        return LLMIG_EINVAL;
+    *out_n = 0;
+    if (m->state != LLMIG_MIGRATION_FINISHED)
+        return LLMIG_EINVAL;
+    const int64_t n = static_cast<int64_t>(m->reserved.size());
+    if (cap < n || (n > 0 && !out))
+        return LLMIG_EINVAL;
+    if (n > 0)
+        std::memcpy(out, m->reserved.data(), static_cast<size_t>(n) * sizeof(int32_t));
+    m->state = LLMIG_MIGRATION_COMMITTED;
+    *out_n = n;
+    return LLMIG_OK;
+}
+
+int llmig_migration_info(const llmig_migration *m, int32_t *state, int64_t *copied_tokens,
+                         int64_t *reserved_blocks, int64_t *stages)
+{
+    if (!m)
+        return LLMIG_EINVAL;
+    if (state)
+        *state = m->state;
+    if (copied_tokens)
+        *copied_tokens = m->copied_tok;
+    if (reserved_blocks)
+        *reserved_blocks = static_cast<int64_t>(m->reserved.size());
+    if (stages)
+        *stages = m->stages;
+    return LLMIG_OK;
 }
 
 int llmig_pack(const llmig_pool *src, const int32_t *blocks, int64_t n, int map_on_device,

@@ -66,6 +66,21 @@ _lib.llmig_write_tokens.argtypes = [_vp, _vp, ctypes.c_int64, ctypes.c_int64, ct
 _lib.llmig_write_tokens.restype = ctypes.c_int
 _lib.llmig_stream_read.argtypes = [_vp, ctypes.c_int64, ctypes.c_int32, ctypes.c_int32, _vp, ctypes.c_int64, _vp]
 _lib.llmig_stream_read.restype = ctypes.c_int
+_lib.llmig_migration_create.argtypes = [ctypes.c_int32, ctypes.POINTER(_vp)]
+_lib.llmig_migration_create.restype = ctypes.c_int
+_lib.llmig_migration_destroy.argtypes = [_vp]
+_lib.llmig_migration_destroy.restype = None
+_lib.llmig_migration_next.argtypes = [_vp, _vp, ctypes.c_int64, ctypes.c_int64, ctypes.c_int, _vp, ctypes.c_int64,
+                                      _vp, _vp, ctypes.c_int64, _i64p]
+_lib.llmig_migration_next.restype = ctypes.c_int
+_lib.llmig_migration_stage.argtypes = [_vp, _vp, _vp, _vp, ctypes.c_int64, ctypes.c_int64, ctypes.c_int, _vp,
+                                       ctypes.c_int64, _vp, _i64p]
+_lib.llmig_migration_stage.restype = ctypes.c_int
+for _name in ("llmig_migration_abort", "llmig_migration_commit"):
+    getattr(_lib, _name).argtypes = [_vp, _vp, ctypes.c_int64, _i64p]
+    getattr(_lib, _name).restype = ctypes.c_int
+_lib.llmig_migration_info.argtypes = [_vp, ctypes.POINTER(ctypes.c_int32), _i64p, _i64p, _i64p]
+_lib.llmig_migration_info.restype = ctypes.c_int
 _lib.llmig_strerror.argtypes = [ctypes.c_int]
 _lib.llmig_strerror.restype = ctypes.c_char_p
 _lib.llmig_last_hip_error.argtypes = []
@@ -215,6 +230,73 @@ def llmig_write_tokens(pool: Pool, table, from_tok: int, data: torch.Tensor, str
     t = _host_i32(table)
     _check(_lib.llmig_write_tokens(pool.handle, t.ctypes.data, t.size, int(from_tok), nbytes // per_tok,
                                    data.data_ptr(), _stream(stream)), "llmig_write_tokens")
+
+
+MIGRATION_STATES = {0: "ACTIVE", 1: "FINISHED", 2: "COMMITTED", 3: "ABORTED"}
+
+
+class MigrationHandle:
+    """The library's migration coordinator (the handshake of Llumnix §4.2):
+    reserves destination blocks stage by stage, aborts with their release,
+    commits after the final stage."""
+
+    def __init__(self, block_size: int):
+        h = _vp()
+        _check(_lib.llmig_migration_create(int(block_size), ctypes.byref(h)), "llmig_migration_create")
+        self._h = h
+        self.block_size = int(block_size)
+
+    def close(self):
+        if getattr(self, "_h", None) is not None:
+            _lib.llmig_migration_destroy(self._h)
+            self._h = None
+
+    def __del__(self):
+        self.close()
+
+    def info(self):
+        st, cp, rs, ns = ctypes.c_int32(), ctypes.c_int64(), ctypes.c_int64(), ctypes.c_int64()
+        _check(_lib.llmig_migration_info(self._h, ctypes.byref(st), ctypes.byref(cp), ctypes.byref(rs),
+                                         ctypes.byref(ns)), "llmig_migration_info")
+        return {"state": MIGRATION_STATES[st.value], "copied_tokens": cp.value, "reserved_blocks": rs.value,
+                "stages": ns.value}
+
+    def next(self, src_table, length: int, final: bool, dst_free_list):
+        """Plan and reserve the next stage without copying; returns (map_src, map_dst)."""
+        st, fl = _host_i32(src_table), _host_i32(dst_free_list)
+        cap = max(fl.size, 1)
+        out_s, out_d = np.empty(cap, np.int32), np.empty(cap, np.int32)
+        n = ctypes.c_int64(0)
+        _check(_lib.llmig_migration_next(self._h, st.ctypes.data, st.size, int(length), int(bool(final)),
+                                         fl.ctypes.data, fl.size, out_s.ctypes.data, out_d.ctypes.data, cap,
+                                         ctypes.byref(n)), "llmig_migration_next")
+        return out_s[:n.value].copy(), out_d[:n.value].copy()
+
+    def stage(self, src: "Pool", dst: "Pool", src_table: np.ndarray, length: int, final: bool,
+              dst_free_list: np.ndarray, stream=None) -> int:
+        """Plan, reserve and launch the next stage; returns the number of
+        free-list entries consumed.  The tables must be contiguous int32."""
+        n = ctypes.c_int64(0)
+        _check(_lib.llmig_migration_stage(self._h, src.handle, dst.handle, src_table.ctypes.data, src_table.size,
+                                          int(length), int(bool(final)), dst_free_list.ctypes.data,
+                                          dst_free_list.size, _stream(stream), ctypes.byref(n)),
+               "llmig_migration_stage")
+        return n.value
+
+    def _take(self, fn, where):
+        cap = max(self.info()["reserved_blocks"], 1)
+        out = np.empty(cap, np.int32)
+        n = ctypes.c_int64(0)
+        _check(fn(self._h, out.ctypes.data, cap, ctypes.byref(n)), where)
+        return out[:n.value].copy()
+
+    def abort(self) -> np.ndarray:
+        """Abort; returns the reserved destination blocks to release."""
+        return self._take(_lib.llmig_migration_abort, "llmig_migration_abort")
+
+    def commit(self) -> np.ndarray:
+        """Commit after the final stage; returns the destination block table."""
+        return self._take(_lib.llmig_migration_commit, "llmig_migration_commit")
 
 
 def llmig_stream_read(region: torch.Tensor, passes: int, workgroups: int, out: torch.Tensor, stream=None) -> None:

@@ -18,12 +18,12 @@ from __future__ import annotations
 
 import math
 import time
-from dataclasses import dataclass, field
+from dataclasses import dataclass
 
 import numpy as np
 import torch
 
-from .llmig import Pool, llmig_pack, llmig_plan, llmig_stage, llmig_unpack, llmig_write_tokens
+from .llmig import MigrationHandle, Pool, llmig_pack, llmig_plan, llmig_unpack, llmig_write_tokens
 
 
 @dataclass
@@ -34,56 +34,68 @@ class StageRecord:
     blocks: int
     final: bool
     gpu_us: float = 0.0
-    map_src: np.ndarray = field(default=None, repr=False)
-    map_dst: np.ndarray = field(default=None, repr=False)
 
 
 class Migration:
-    """Bookkeeping of one request's migration: which tokens are copied, which
-    destination blocks were reserved, and the stages so far."""
+    """One request's migration, driven through the library's coordinator
+    (which plans, reserves destination blocks and launches each stage in one
+    call).  Keeps the host-side records: the stages so far, their GPU times,
+    and which destination blocks were consumed from the free list."""
 
     def __init__(self, src: Pool, dst: Pool, src_table, dst_free_list, stream: torch.cuda.Stream):
         self.src, self.dst, self.stream = src, dst, stream
         self.bs = src.block_size
         self.src_table = np.ascontiguousarray(np.asarray(src_table, dtype=np.int32))
-        self.free = np.ascontiguousarray(np.asarray(dst_free_list, dtype=np.int32))
+        self._free0 = np.ascontiguousarray(np.asarray(dst_free_list, dtype=np.int32))
+        self._consumed = 0
         self.copied_tok = 0
-        self._dst_parts: list[np.ndarray] = []
         self.stages: list[StageRecord] = []
         self._events = []
+        self.coord = MigrationHandle(self.bs)
+
+    @property
+    def free(self) -> np.ndarray:
+        """What is left of the destination free list."""
+        return self._free0[self._consumed:]
 
     @property
     def dst_table(self) -> np.ndarray:
-        """Destination block of every logical block copied so far."""
-        if not self._dst_parts:
-            return np.zeros(0, np.int32)
-        return np.concatenate(self._dst_parts)
+        """Destination block of every logical block copied so far (the
+        consumed head of the free list, in logical order)."""
+        return self._free0[:self._consumed]
 
     def remaining_blocks(self, length: int) -> int:
         return math.ceil(length / self.bs) - self.copied_tok // self.bs
 
     def stage(self, length: int, final: bool, time_it: bool = True) -> StageRecord:
-        """Plan and launch the next stage for a request that now holds
-        ``length`` tokens.  A non-final stage stops at the last whole block."""
-        end = length if final else (length // self.bs) * self.bs
-        ms, md = llmig_plan(self.src_table, self.free, length, self.copied_tok, end, self.bs)
+        """Plan, reserve and launch the next stage for a request that now
+        holds ``length`` tokens.  A non-final stage stops at the last whole
+        block."""
         ev = None
         if time_it:
             ev = (torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
             ev[0].record(self.stream)
-        llmig_stage(self.src, self.dst, ms, md, stream=self.stream)
+        n = self.coord.stage(self.src, self.dst, self.src_table, length, final, self.free, stream=self.stream)
         if time_it:
             ev[1].record(self.stream)
-        rec = StageRecord(length, self.copied_tok, end, len(md), final, map_src=ms, map_dst=md)
+        end = length if final else (length // self.bs) * self.bs
+        rec = StageRecord(length, self.copied_tok, end, n, final)
         self.stages.append(rec)
         self._events.append(ev)
-        self.free = self.free[len(md):]
-        self._dst_parts.append(md)
+        self._consumed += n
         self.copied_tok = end
         return rec
 
+    def abort(self) -> np.ndarray:
+        """Abort: the destination blocks reserved so far, to be released."""
+        return self.coord.abort()
+
+    def commit(self) -> np.ndarray:
+        """Commit after the final stage: the request's destination table."""
+        return self.coord.commit()
+
     def collect_times(self) -> None:
-        """Fill in each stage's GPU time (call after the stream is synchronised)."""
+        """Fill in each timed stage's GPU time (after the stream is synchronised)."""
         for rec, ev in zip(self.stages, self._events):
             if ev is not None:
                 rec.gpu_us = ev[0].elapsed_time(ev[1]) * 1e3

@@ -293,3 +293,44 @@ def test_errors_have_no_effect():
     llmig.llmig_pack(src, np.zeros(0, np.int32), good)
     torch.cuda.synchronize()
     assert_same(host_image(dst), before, "destination after empty calls")
+
+
+# ------------------------------------------------------------------- coordinator: abort and commit
+def test_coordinator_abort_leaves_unreserved_blocks_untouched():
+    shape = wl.PoolShape(3, 200, 16, 4, 64, "fp16")
+    say("coordinator abort", shape)
+    src = make_pool(shape, 88, wl.SRC_VALUES)
+    dst = make_pool(shape, 88, wl.DST_VALUES)
+    table, _ = wl.request_table(88, shape.num_blocks, 40)
+    free, _ = wl.free_list(88, shape.num_blocks)
+    hs, hd = host_image(src), host_image(dst)
+    mig = torch.cuda.Stream()
+    m = migrate.Migration(src, dst, table, free, mig)
+    m.stage(400, final=False)             # 25 blocks
+    m.stage(430, final=False)             # 1 more block
+    mig.synchronize()
+    released = m.abort()
+    assert np.array_equal(released, free[:26])
+    torch.cuda.synchronize()
+    # reserved blocks hold the copies made so far; every other block is untouched
+    oracle.default().copy(hs, hd, table[:26], free[:26])
+    assert_same(host_image(dst), hd, "destination after abort")
+    with pytest.raises(LlmigError):
+        m.stage(440, final=True)          # nothing may follow an abort
+
+
+def test_coordinator_commit_table():
+    shape = wl.PoolShape(2, 100, 16, 2, 64, "bf16")
+    say("coordinator commit", shape)
+    src = make_pool(shape, 89, wl.SRC_VALUES)
+    dst = make_pool(shape, 89, wl.DST_VALUES)
+    table, _ = wl.request_table(89, shape.num_blocks, 30)
+    free, _ = wl.free_list(89, shape.num_blocks)
+    mig = torch.cuda.Stream()
+    m = migrate.Migration(src, dst, table, free, mig)
+    m.stage(200, final=False)
+    m.stage(233, final=True)
+    mig.synchronize()
+    got = m.commit()
+    assert np.array_equal(got, free[:15]) and np.array_equal(got, m.dst_table)
+    assert oracle.default().first_token_mismatch(host_image(src), table, host_image(dst), got, 233) == -1
