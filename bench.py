@@ -339,20 +339,23 @@ def batched_section(reps=10, host_reps=3, chunk_pairs=64):
                        "max": int(max(su.lengths)), "tokens": int(sum(su.lengths))}}
     chunk_bytes = chunk_pairs * shape.num_layers * 2 * src.tile_bytes
     bufs = [torch.empty(chunk_bytes, dtype=torch.uint8, pin_memory=True) for _ in range(2)]
+    dev_bufs = [(torch.empty(chunk_bytes, dtype=torch.uint8, device="cuda"),
+                 torch.empty(chunk_bytes, dtype=torch.uint8, device="cuda")) for _ in range(2)]
     ps, us_ = torch.cuda.Stream(), torch.cuda.Stream()
-    host_times = []
-    for r in range(host_reps + 1):
-        torch.cuda.synchronize()
-        t0 = time.perf_counter()
-        migrate.run_host_staged(src, dst, ms, md, bufs, ps, us_, chunk_pairs)
-        torch.cuda.synchronize()
-        if r:
-            host_times.append(time.perf_counter() - t0)
-    ht = statistics.median(host_times)
     one_way = len(ms) * shape.num_layers * 2 * src.tile_bytes
-    out["host_staged"] = {"chunk_pairs": chunk_pairs, "seconds_median": round(ht, 4),
-                          "bytes_each_way": one_way, "GBps_each_way": round(one_way / ht / 1e9, 2),
+    out["host_staged"] = {"chunk_pairs": chunk_pairs, "bytes_each_way": one_way,
                           "bound": "PCIe Gen5 x16, ~64 GB/s per direction"}
+    for mode, db in (("kernel_pcie", None), ("copy_engine", dev_bufs)):
+        host_times = []
+        for r in range(host_reps + 1):
+            torch.cuda.synchronize()
+            t0 = time.perf_counter()
+            migrate.run_host_staged(src, dst, ms, md, bufs, ps, us_, chunk_pairs, dev_bufs=db)
+            torch.cuda.synchronize()
+            if r:
+                host_times.append(time.perf_counter() - t0)
+        ht = statistics.median(host_times)
+        out["host_staged"][mode] = {"seconds_median": round(ht, 4), "GBps_each_way": round(one_way / ht / 1e9, 2)}
     su.close()
     return out
 

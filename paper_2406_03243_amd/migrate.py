@@ -202,26 +202,44 @@ def plan_batch(tables, lengths, dst_free_list, block_size: int):
 
 
 def run_host_staged(src: Pool, dst: Pool, map_src, map_dst, host_bufs, pack_stream, unpack_stream,
-                    chunk_pairs: int):
+                    chunk_pairs: int, dev_bufs=None):
     """Block fusion through pinned host memory (Llumnix §5): chunks of
-    ``chunk_pairs`` block pairs are packed from the source pool into one of
-    two pinned host buffers (the kernel stores over PCIe) and unpacked from
-    it into the destination pool (the kernel loads over PCIe), the two
-    buffers alternating so that packing chunk k+1 overlaps unpacking chunk k.
-    Events order each unpack after its pack and each reuse of a buffer after
-    the unpack that read it.  Returns once all work is enqueued."""
+    ``chunk_pairs`` block pairs go from the source pool to one of two pinned
+    host buffers and from there into the destination pool, the two buffers
+    alternating so that one chunk's way out overlaps the previous chunk's way
+    in.  Events order each unpack after its pack and each reuse of a buffer
+    after the work that read it.
+
+    Without ``dev_bufs`` the pack kernel stores straight into the pinned
+    buffer and the unpack kernel loads straight from it, over PCIe.  With
+    ``dev_bufs`` (two pairs of device buffers of the same size) the kernels
+    pack into and unpack from device memory and the copy engines move the
+    buffers across PCIe (hipMemcpyAsync).  Returns once all work is enqueued."""
     n = len(map_src)
-    unpacked = [None, None]
+    freed = [None, None]                 # event after which host buffer k may be rewritten
     for c, lo in enumerate(range(0, n, chunk_pairs)):
         hi = min(n, lo + chunk_pairs)
-        buf = host_bufs[c % 2]
-        if unpacked[c % 2] is not None:
-            pack_stream.wait_event(unpacked[c % 2])
-        llmig_pack(src, map_src[lo:hi], buf, stream=pack_stream)
+        k = c % 2
+        host = host_bufs[k]
+        if freed[k] is not None:
+            pack_stream.wait_event(freed[k])
+        if dev_bufs is None:
+            llmig_pack(src, map_src[lo:hi], host, stream=pack_stream)
+        else:
+            out_dev, in_dev = dev_bufs[k]
+            llmig_pack(src, map_src[lo:hi], out_dev, stream=pack_stream)
+            nbytes = (hi - lo) * src.num_layers * 2 * src.tile_bytes
+            with torch.cuda.stream(pack_stream):
+                host[:nbytes].copy_(out_dev[:nbytes], non_blocking=True)
         packed = torch.cuda.Event()
         packed.record(pack_stream)
         unpack_stream.wait_event(packed)
-        llmig_unpack(dst, map_dst[lo:hi], buf, stream=unpack_stream)
+        if dev_bufs is None:
+            llmig_unpack(dst, map_dst[lo:hi], host, stream=unpack_stream)
+        else:
+            with torch.cuda.stream(unpack_stream):
+                in_dev[:nbytes].copy_(host[:nbytes], non_blocking=True)
+            llmig_unpack(dst, map_dst[lo:hi], in_dev, stream=unpack_stream)
         ev = torch.cuda.Event()
         ev.record(unpack_stream)
-        unpacked[c % 2] = ev
+        freed[k] = ev

@@ -159,9 +159,10 @@ def test_batched_one_call_full():
     su.close()
 
 
-def test_batched_host_staged_full():
+@pytest.mark.parametrize("mode", ["kernel_pcie", "copy_engine"])
+def test_batched_host_staged_full(mode):
     su = scenarios.batched()
-    say("batched host staged", su.shape)
+    say("batched host staged", mode, su.shape)
     ms, md, _ = migrate.plan_batch(su.tables, su.lengths, su.free, su.shape.block_size)
     sample = np.sort(wl.stream(su.workload.seed, wl.EXTRA, 4).choice(len(ms), 128, replace=False))
     hs = compact(su.src, ms[sample])
@@ -171,7 +172,12 @@ def test_batched_host_staged_full():
     chunk = 64
     nbytes = chunk * su.shape.num_layers * 2 * su.src.tile_bytes
     bufs = [torch.empty(nbytes, dtype=torch.uint8, pin_memory=True) for _ in range(2)]
-    migrate.run_host_staged(su.src, su.dst, ms, md, bufs, torch.cuda.Stream(), torch.cuda.Stream(), chunk)
+    dev_bufs = None
+    if mode == "copy_engine":
+        dev_bufs = [(torch.empty(nbytes, dtype=torch.uint8, device="cuda"),
+                     torch.empty(nbytes, dtype=torch.uint8, device="cuda")) for _ in range(2)]
+    migrate.run_host_staged(su.src, su.dst, ms, md, bufs, torch.cuda.Stream(), torch.cuda.Stream(), chunk,
+                            dev_bufs=dev_bufs)
     torch.cuda.synchronize()
     ids = np.arange(len(sample), dtype=np.int32)
     oracle.default().copy(hs, hd, ids, ids)
