@@ -38,16 +38,24 @@ def log(*a):
     print("[bench]", *a, file=sys.stderr, flush=True)
 
 
+def copy_kernel_hash() -> str:
+    """sha256 of the copy kernel's sources (its device code and launch
+    configuration: csrc/common.h followed by csrc/copy_tiles.h)."""
+    import hashlib
+    h = hashlib.sha256()
+    for name in ("common.h", "copy_tiles.h"):
+        h.update(open(os.path.join(ROOT, "paper_2406_03243_amd", "csrc", name), "rb").read())
+    return h.hexdigest()
+
+
 def recorded_traffic(kernel: str):
     """HBM bytes per launch of ``kernel`` from the committed counter summary
     (two rocprofv3 --pmc passes, calibrated against a plain copy), or None
     when the kernel source has changed since the counters were taken."""
-    import hashlib
     path = os.path.join(ROOT, "profiles", "copy_tiles_bulk_llama7b_traffic.txt")
-    src = os.path.join(ROOT, "paper_2406_03243_amd", "csrc", "llmig.hip")
     try:
         rec = json.load(open(path))
-        now = hashlib.sha256(open(src, "rb").read()).hexdigest()
+        now = copy_kernel_hash()
     except (OSError, ValueError):
         return None
     if rec.get("kernel") != kernel or rec.get("kernel_source_sha256") != now:
@@ -360,9 +368,10 @@ def batched_section(reps=10, host_reps=3, chunk_pairs=64):
     return out
 
 
-def load_section(reps=3, reader_passes=3, step_ms=20.0):
+def load_section(reps=3, reader_passes=3, step_ms=20.0, caps=(0, 256, 64)):
     """GQA long-context migration beside a streaming reader of a separate
-    40 GB region (all streams at the default priority)."""
+    40 GB region (all streams at the default priority), for several caps on
+    the migration's copy grid (0: uncapped)."""
     import torch
 
     from paper_2406_03243_amd import migrate, scenarios
@@ -377,6 +386,7 @@ def load_section(reps=3, reader_passes=3, step_ms=20.0):
     sink = torch.empty(wgs * 256, dtype=torch.int64, device="cuda")
     rd, mig, dec = torch.cuda.Stream(), torch.cuda.Stream(), torch.cuda.Stream()
     length = su.lengths[0]
+    read_bytes = reader_passes * region.numel() * region.element_size()
 
     def reader_run():
         e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
@@ -385,46 +395,48 @@ def load_section(reps=3, reader_passes=3, step_ms=20.0):
         e1.record(rd)
         return e0, e1
 
-    # alone: reader, then migration
-    alone_r, alone_m = [], []
+    alone_r = []
     for r in range(reps + 1):
         e = reader_run()
         torch.cuda.synchronize()
         if r:
             alone_r.append(e[0].elapsed_time(e[1]) * 1e3)
-    for r in range(reps + 1):
-        m, dt = migrate.run_timed(src, dst, table, length, free, append_pool, mig, dec, step_ms=step_ms)
-        if r:
-            alone_m.append((m, dt))
-    # together: the reader starts, then the migration
-    both = []
-    for r in range(reps + 1):
-        torch.cuda.synchronize()
-        e = reader_run()
-        t0 = time.perf_counter()
-        m, dt = migrate.run_timed(src, dst, table, length, free, append_pool, mig, dec, step_ms=step_ms)
-        t_mig = time.perf_counter() - t0
-        torch.cuda.synchronize()
-        if r:
-            both.append((e[0].elapsed_time(e[1]) * 1e3, m, dt, t_mig))
-    read_bytes = reader_passes * region.numel() * region.element_size()
     r_alone = statistics.median(alone_r)
-    r_both = statistics.median(b[0] for b in both)
-    t_mig = statistics.median(b[3] for b in both) * 1e6
-    s1_bytes = stage_bytes(alone_m[0][0].stages[0].blocks, shape, src.tile_bytes)
-    s1_alone = statistics.median(m.stages[0].gpu_us for m, _ in alone_m)
-    s1_both = statistics.median(b[1].stages[0].gpu_us for b in both)
     out = {"workload": su.workload.name, "tokens": length, "reader_bytes": read_bytes,
-           "reader_workgroups": wgs,
-           "reader_alone_GBps": round(read_bytes / (r_alone * 1e-6) / 1e9, 1),
-           "reader_with_migration_GBps": round(read_bytes / (r_both * 1e-6) / 1e9, 1),
-           "reader_slowdown_during_migration": round(max(0.0, r_both - r_alone) / t_mig, 3),
-           "migration_wall_us": round(t_mig, 1),
-           "stage1_GBps_alone": round(s1_bytes / (s1_alone * 1e-6) / 1e9, 1),
-           "stage1_GBps_under_load": round(s1_bytes / (s1_both * 1e-6) / 1e9, 1),
-           "stages_under_load": statistics.median(len(b[1].stages) for b in both),
-           "downtime_us_alone": round(statistics.median(dt for _, dt in alone_m), 1),
-           "downtime_us_under_load": round(statistics.median(b[2] for b in both), 1)}
+           "reader_workgroups": wgs, "reader_alone_GBps": round(read_bytes / (r_alone * 1e-6) / 1e9, 1),
+           "by_cap": {}}
+    for cap in caps:
+        alone_m = []
+        for r in range(reps + 1):
+            m, dt = migrate.run_timed(src, dst, table, length, free, append_pool, mig, dec, step_ms=step_ms,
+                                      max_workgroups=cap)
+            if r:
+                alone_m.append((m, dt))
+        both = []
+        for r in range(reps + 1):
+            torch.cuda.synchronize()
+            e = reader_run()
+            t0 = time.perf_counter()
+            m, dt = migrate.run_timed(src, dst, table, length, free, append_pool, mig, dec, step_ms=step_ms,
+                                      max_workgroups=cap)
+            t_mig = time.perf_counter() - t0
+            torch.cuda.synchronize()
+            if r:
+                both.append((e[0].elapsed_time(e[1]) * 1e3, m, dt, t_mig))
+        r_both = statistics.median(b[0] for b in both)
+        t_mig = statistics.median(b[3] for b in both) * 1e6
+        s1_bytes = stage_bytes(alone_m[0][0].stages[0].blocks, shape, src.tile_bytes)
+        s1_alone = statistics.median(m.stages[0].gpu_us for m, _ in alone_m)
+        s1_both = statistics.median(b[1].stages[0].gpu_us for b in both)
+        out["by_cap"][str(cap) if cap else "uncapped"] = {
+            "reader_with_migration_GBps": round(read_bytes / (r_both * 1e-6) / 1e9, 1),
+            "reader_slowdown_during_migration": round(max(0.0, r_both - r_alone) / t_mig, 3),
+            "migration_wall_us": round(t_mig, 1),
+            "stage1_GBps_alone": round(s1_bytes / (s1_alone * 1e-6) / 1e9, 1),
+            "stage1_GBps_under_load": round(s1_bytes / (s1_both * 1e-6) / 1e9, 1),
+            "stages_under_load": statistics.median(len(b[1].stages) for b in both),
+            "downtime_us_alone": round(statistics.median(dt for _, dt in alone_m), 1),
+            "downtime_us_under_load": round(statistics.median(b[2] for b in both), 1)}
     su.close()
     return out
 

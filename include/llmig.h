@@ -222,6 +222,16 @@ int llmig_migration_stage(llmig_migration *m, const llmig_pool *src, const llmig
                           const int32_t *src_table, int64_t src_table_len, int64_t len, int final_stage,
                           const int32_t *dst_free_list, int64_t dst_free_len, void *stream, int64_t *out_n);
 
+/* Caps the number of workgroups the migration's non-final stages launch
+ * (0, the default, means one per work item); the final stage is the
+ * request's downtime and always runs uncapped.  A capped grid keeps fewer workgroups
+ * resident, which leaves CUs and HBM bandwidth to the decode work running
+ * beside the migration at the cost of a slower copy: the lever for the
+ * paper's goal of near-zero overhead on running requests (§6.2), since
+ * stream priorities do not preempt running workgroups.  LLMIG_EINVAL for a
+ * negative value. */
+int llmig_migration_set_max_workgroups(llmig_migration *m, int32_t max_workgroups);
+
 /* Aborts (ACTIVE or FINISHED): writes every reserved destination block to
  * out (capacity cap; *out_n = count) so the destination can release them,
  * and moves to ABORTED.  Copies already enqueued may still write into those

@@ -79,6 +79,8 @@ _lib.llmig_migration_stage.restype = ctypes.c_int
 for _name in ("llmig_migration_abort", "llmig_migration_commit"):
     getattr(_lib, _name).argtypes = [_vp, _vp, ctypes.c_int64, _i64p]
     getattr(_lib, _name).restype = ctypes.c_int
+_lib.llmig_migration_set_max_workgroups.argtypes = [_vp, ctypes.c_int32]
+_lib.llmig_migration_set_max_workgroups.restype = ctypes.c_int
 _lib.llmig_migration_info.argtypes = [_vp, ctypes.POINTER(ctypes.c_int32), _i64p, _i64p, _i64p]
 _lib.llmig_migration_info.restype = ctypes.c_int
 _lib.llmig_strerror.argtypes = [ctypes.c_int]
@@ -253,6 +255,10 @@ class MigrationHandle:
 
     def __del__(self):
         self.close()
+
+    def set_max_workgroups(self, n: int) -> None:
+        """Cap the copy grid (0: uncapped) to leave bandwidth to decoding."""
+        _check(_lib.llmig_migration_set_max_workgroups(self._h, int(n)), "llmig_migration_set_max_workgroups")
 
     def info(self):
         st, cp, rs, ns = ctypes.c_int32(), ctypes.c_int64(), ctypes.c_int64(), ctypes.c_int64()

@@ -42,7 +42,8 @@ class Migration:
     call).  Keeps the host-side records: the stages so far, their GPU times,
     and which destination blocks were consumed from the free list."""
 
-    def __init__(self, src: Pool, dst: Pool, src_table, dst_free_list, stream: torch.cuda.Stream):
+    def __init__(self, src: Pool, dst: Pool, src_table, dst_free_list, stream: torch.cuda.Stream,
+                 max_workgroups: int = 0):
         self.src, self.dst, self.stream = src, dst, stream
         self.bs = src.block_size
         self.src_table = np.ascontiguousarray(np.asarray(src_table, dtype=np.int32))
@@ -52,6 +53,8 @@ class Migration:
         self.stages: list[StageRecord] = []
         self._events = []
         self.coord = MigrationHandle(self.bs)
+        if max_workgroups:
+            self.coord.set_max_workgroups(max_workgroups)
 
     @property
     def free(self) -> np.ndarray:
@@ -146,14 +149,15 @@ def run_scheduled(src: Pool, dst: Pool, src_table, dst_free_list, initial_len: i
 
 def run_timed(src: Pool, dst: Pool, src_table, initial_len: int, dst_free_list, append_pool,
               mig_stream, dec_stream, step_ms: float = 20.0, last_stage_max_blocks: int = 1,
-              max_stages: int = 8):
+              max_stages: int = 8, max_workgroups: int = 0):
     """A migration whose decoding speed is simulated: while a stage copies,
     decoding produces max(1, ceil(stage_time / step_ms)) tokens, which are
     written once the stage is over.  The next stage is final when at most
     ``last_stage_max_blocks`` blocks remain, or at ``max_stages``.
     ``append_pool`` is a device tensor [L][K,V][max_tokens][slot_bytes] the
-    appended tokens are drawn from.  Returns (migration, downtime_us)."""
-    m = Migration(src, dst, src_table, dst_free_list, mig_stream)
+    appended tokens are drawn from.  ``max_workgroups`` caps the copy grid
+    (0: uncapped).  Returns (migration, downtime_us)."""
+    m = Migration(src, dst, src_table, dst_free_list, mig_stream, max_workgroups)
     length = initial_len
     max_tok = append_pool.shape[2]
     used = 0

@@ -334,3 +334,25 @@ def test_coordinator_commit_table():
     got = m.commit()
     assert np.array_equal(got, free[:15]) and np.array_equal(got, m.dst_table)
     assert oracle.default().first_token_mismatch(host_image(src), table, host_image(dst), got, 233) == -1
+
+
+@pytest.mark.parametrize("cap", [1, 7, 64])
+def test_capped_grid_multistage(cap):
+    """Throttled migrations: a capped grid walks many items per workgroup."""
+    shape = wl.PoolShape(5, 300, 16, 13, 128, "fp16")       # 52 KiB tiles: 13 rows, two chunks
+    say("capped grid", cap, shape)
+    src = make_pool(shape, 90 + cap, wl.SRC_VALUES)
+    dst = make_pool(shape, 90 + cap, wl.DST_VALUES)
+    table, _ = wl.request_table(90 + cap, shape.num_blocks, 120)
+    free, _ = wl.free_list(90 + cap, shape.num_blocks)
+    hs, hd = host_image(src), host_image(dst)
+    mig = torch.cuda.Stream()
+    m = migrate.Migration(src, dst, table, free, mig, max_workgroups=cap)
+    m.stage(1500, final=False)
+    m.stage(1700, final=False)
+    m.stage(1709, final=True)
+    mig.synchronize()
+    got = m.commit()
+    oracle.default().copy(hs, hd, table[:len(got)], got)
+    assert_same(host_image(dst), hd, "destination")
+    assert oracle.default().first_token_mismatch(hs, table, host_image(dst), got, 1709) == -1
