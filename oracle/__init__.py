@@ -37,7 +37,7 @@ def build(source: str = SOURCE, library: str = LIBRARY, quiet: bool = False) -> 
     """Compile the C oracle with gcc into a shared library; returns its path."""
     tmp = library + ".tmp"
     warn = ["-w"] if quiet else ["-Wall", "-Wextra"]
-    subprocess.run(["gcc", "-O2", "-std=c11", *warn, "-shared", "-fPIC", "-o", tmp, source],
+    subprocess.run(["gcc", "-O2", "-std=c11", *warn, "-shared", "-fPIC", "-o", tmp, source, "-lm"],
                    check=True)
     os.replace(tmp, library)
     return library
@@ -130,6 +130,15 @@ class Oracle:
         lib.oracle_first_token_mismatch.argtypes = [_pp, _pp, _i32p, _pp, _pp, _i32p,
                                                     ctypes.c_int32, ctypes.c_int32, ctypes.c_int64,
                                                     ctypes.c_int64]
+        lib.oracle_half_to_double.restype = ctypes.c_double
+        lib.oracle_half_to_double.argtypes = [ctypes.c_uint16]
+        lib.oracle_bf16_to_double.restype = ctypes.c_double
+        lib.oracle_bf16_to_double.argtypes = [ctypes.c_uint16]
+        lib.oracle_decode_attention.restype = None
+        lib.oracle_decode_attention.argtypes = [_pp, _pp, ctypes.c_int32, ctypes.c_int32, ctypes.c_int32,
+                                                ctypes.c_int32, ctypes.c_int, ctypes.c_void_p, ctypes.c_int32,
+                                                ctypes.c_int32, _i32p, ctypes.c_int32, _i32p, ctypes.c_double,
+                                                ctypes.c_void_p]
         self.lib = lib
 
     # ---- one stage's plan (Llumnix §4.2, pre-allocation before each stage) ----
@@ -215,6 +224,36 @@ class Oracle:
         return self.lib.oracle_first_token_mismatch(ak, av, ta.ctypes.data_as(_i32p), bk, bv,
                                                     tb.ctypes.data_as(_i32p), a.num_layers,
                                                     a.block_size, a.slot_bytes, length)
+
+    # ---- decode attention over the paged pool (the work beside a migration) ----
+    def half_to_double(self, bits: int) -> float:
+        return self.lib.oracle_half_to_double(bits)
+
+    def bf16_to_double(self, bits: int) -> float:
+        return self.lib.oracle_bf16_to_double(bits)
+
+    def decode_attention(self, pool: HostPool, kv_heads: int, head_dim: int, dtype: str, q: np.ndarray,
+                         tables: np.ndarray, ctx, scale: float) -> np.ndarray:
+        """q: uint16 bits [L][B][Hq][D]; tables: int32 [B][stride]; ctx: [B].
+        Returns float64 [L][B][Hq][D]."""
+        q = np.ascontiguousarray(q, dtype=np.uint16)
+        num_layers, batch, q_heads, d = q.shape
+        assert num_layers == pool.num_layers and d == head_dim and q_heads % kv_heads == 0
+        assert pool.slot_bytes == kv_heads * head_dim * 2
+        t = np.ascontiguousarray(tables, dtype=np.int32)
+        c = _i32(ctx)
+        assert t.shape[0] == batch and len(c) == batch
+        for b in range(batch):
+            if c[b] > 0:
+                need = (c[b] - 1) // pool.block_size + 1
+                assert need <= t.shape[1] and t[b, :need].min() >= 0 and t[b, :need].max() < pool.num_blocks
+        out = np.zeros((num_layers, batch, q_heads, head_dim), np.float64)
+        k, v = pool._ptrs()
+        self.lib.oracle_decode_attention(k, v, num_layers, pool.block_size, kv_heads, head_dim,
+                                         1 if dtype == "bf16" else 0, q.ctypes.data, batch, q_heads,
+                                         t.ctypes.data_as(_i32p), t.shape[1], c.ctypes.data_as(_i32p),
+                                         float(scale), out.ctypes.data)
+        return out
 
     # ---- multi-stage migration (Llumnix §4.2) ----
     def migrate(self, src: HostPool, dst: HostPool, src_table, dst_free_list, events):

@@ -34,6 +34,7 @@
  * stage needs: the failed pre-allocation of the handshake, Llumnix §4.2),
  * ORACLE_ERANGE (a negative block id).
  */
+#include <math.h>
 #include <stdint.h>
 #include <string.h>
 
@@ -261,4 +262,99 @@ int64_t oracle_first_token_mismatch(uint8_t *const *a_k, uint8_t *const *a_v,
         }
     }
     return -1;
+}
+
+/* ------------------------------------------------------------------------
+ * Decode attention over the paged pool (the work that runs beside a
+ * migration and whose slowdown Llumnix §6.2 measures).  For every layer l,
+ * sequence b and query head h (served by KV head g = h / (q_heads /
+ * kv_heads), grouped-query attention), with the sequence's ctx tokens
+ * reached through its block table:
+ *     s_t = scale * sum_d q[l][b][h][d] * K_l[t][g][d]
+ *     p_t = exp(s_t - max_t s) / sum_t exp(s_t - max_t s)
+ *     out[l][b][h][d] = sum_t p_t * V_l[t][g][d]
+ * in double precision; a sequence with ctx = 0 gives zeros.
+ * ---------------------------------------------------------------------- */
+
+/* IEEE 754 binary16 bits to double, from the format: 1 sign bit, 5 exponent
+ * bits (bias 15), 10 fraction bits; exponent 0 encodes zero and subnormals,
+ * 31 infinities and NaNs. */
+double oracle_half_to_double(uint16_t h)
+{
+    int sign = (h >> 15) & 1;
+    int exp = (h >> 10) & 0x1f;
+    int frac = h & 0x3ff;
+    double v;
+    if (exp == 0)
+        v = ldexp((double)frac, -24);
+    else if (exp == 31)
+        v = frac ? NAN : INFINITY;
+    else
+        v = ldexp((double)(frac | 0x400), exp - 25);
+    return sign ? -v : v;
+}
+
+/* bfloat16 bits to double: the upper half of an IEEE binary32. */
+double oracle_bf16_to_double(uint16_t h)
+{
+    uint32_t bits = (uint32_t)h << 16;
+    float f;
+    memcpy(&f, &bits, sizeof f);
+    return (double)f;
+}
+
+static double elem(const uint8_t *base, int64_t index, int is_bf16)
+{
+    uint16_t bits;
+    memcpy(&bits, base + index * 2, 2);
+    return is_bf16 ? oracle_bf16_to_double(bits) : oracle_half_to_double(bits);
+}
+
+/* q: [num_layers][batch][q_heads][head_dim] 16-bit; tables: [batch][table_stride]
+ * block ids; ctx: [batch]; out: [num_layers][batch][q_heads][head_dim] double. */
+void oracle_decode_attention(uint8_t *const *pool_k, uint8_t *const *pool_v, int32_t num_layers,
+                             int32_t block_size, int32_t kv_heads, int32_t head_dim, int is_bf16,
+                             const uint8_t *q, int32_t batch, int32_t q_heads,
+                             const int32_t *tables, int32_t table_stride, const int32_t *ctx,
+                             double scale, double *out)
+{
+    int32_t group = q_heads / kv_heads;
+    for (int32_t l = 0; l < num_layers; l++) {
+        for (int32_t b = 0; b < batch; b++) {
+            for (int32_t h = 0; h < q_heads; h++) {
+                int32_t g = h / group;
+                int64_t qoff = (((int64_t)l * batch + b) * q_heads + h) * head_dim;
+                double *o = out + qoff;
+                for (int32_t d = 0; d < head_dim; d++)
+                    o[d] = 0.0;
+                if (ctx[b] <= 0)
+                    continue;
+                double smax = -INFINITY;
+                for (int32_t t = 0; t < ctx[b]; t++) {
+                    int64_t row = ((int64_t)tables[(int64_t)b * table_stride + t / block_size] * block_size
+                                   + t % block_size) * kv_heads + g;
+                    double s = 0.0;
+                    for (int32_t d = 0; d < head_dim; d++)
+                        s += elem(q, qoff + d, is_bf16) * elem(pool_k[l], row * head_dim + d, is_bf16);
+                    s *= scale;
+                    if (s > smax)
+                        smax = s;
+                }
+                double denom = 0.0;
+                for (int32_t t = 0; t < ctx[b]; t++) {
+                    int64_t row = ((int64_t)tables[(int64_t)b * table_stride + t / block_size] * block_size
+                                   + t % block_size) * kv_heads + g;
+                    double s = 0.0;
+                    for (int32_t d = 0; d < head_dim; d++)
+                        s += elem(q, qoff + d, is_bf16) * elem(pool_k[l], row * head_dim + d, is_bf16);
+                    double w = exp(s * scale - smax);
+                    denom += w;
+                    for (int32_t d = 0; d < head_dim; d++)
+                        o[d] += w * elem(pool_v[l], row * head_dim + d, is_bf16);
+                }
+                for (int32_t d = 0; d < head_dim; d++)
+                    o[d] /= denom;
+            }
+        }
+    }
 }

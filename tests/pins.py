@@ -22,7 +22,13 @@ What pins what:
   * appends  - numpy indexing of the [num_blocks, block_size, slot] view;
   * identity - planted single-byte differences are found at their token;
   * stages   - a whole multi-stage replay ends with every token identical,
-               ceil(len/bs) blocks, stages partitioning the block set.
+               ceil(len/bs) blocks, stages partitioning the block set;
+  * 16-bit   - fp16 and bf16 decoding against numpy/torch for all 65536
+               bit patterns;
+  * decode attention - dense torch float64 softmax attention over the
+               gathered sequence; one token gives its V row; zero scale
+               gives the mean of V; grouped heads read their own KV head;
+               moving the tokens between blocks leaves the output unchanged.
 """
 from __future__ import annotations
 
@@ -337,6 +343,117 @@ def pin_multistage_replay(orc):
         # non-final stages hold whole blocks only
         for length, lo, hi in bounds[:-1]:
             assert lo % bs == 0 and hi % bs == 0
+
+
+# --------------------------------------------------------------------------- decode attention
+def pin_16bit_conversions_exhaustive(orc):
+    bits = np.arange(65536, dtype=np.uint32).astype(np.uint16)
+    want_h = bits.view(np.float16).astype(np.float64)
+    want_b = torch.from_numpy(bits.view(np.int16)).view(torch.bfloat16).double().numpy()
+    got_h = np.array([orc.half_to_double(int(b)) for b in bits])
+    got_b = np.array([orc.bf16_to_double(int(b)) for b in bits])
+    for got, want in ((got_h, want_h), (got_b, want_b)):
+        nan = np.isnan(want)
+        assert np.array_equal(np.isnan(got), nan)
+        assert np.array_equal(got[~nan], want[~nan])
+
+
+def _attn_case(rng, num_layers, nb, bs, kv_heads, head_dim, group, ctx, dtype):
+    """A random pool, queries and block tables for decode attention."""
+    slot = kv_heads * head_dim * 2
+    t = bs * slot
+    vals = rng.uniform(-1, 1, size=(2, num_layers, nb, t // 2))
+    if dtype == "fp16":
+        bits = vals.astype(np.float16).view(np.uint16)
+    else:
+        bits = torch.from_numpy(vals.astype(np.float32)).to(torch.bfloat16).view(torch.int16).numpy().view(np.uint16)
+    pool = HostPool([np.ascontiguousarray(bits[0, l]).view(np.uint8) for l in range(num_layers)],
+                    [np.ascontiguousarray(bits[1, l]).view(np.uint8) for l in range(num_layers)], bs, slot)
+    batch = len(ctx)
+    stride = max(1, max(-(-c // bs) for c in ctx))
+    tables = np.stack([rng.choice(nb, stride, replace=False) for _ in range(batch)]).astype(np.int32)
+    qv = rng.uniform(-1, 1, size=(num_layers, batch, kv_heads * group, head_dim))
+    if dtype == "fp16":
+        q = qv.astype(np.float16).view(np.uint16)
+    else:
+        q = torch.from_numpy(qv.astype(np.float32)).to(torch.bfloat16).view(torch.int16).numpy().view(np.uint16)
+    return pool, q, tables
+
+
+def _dense(pool, layer, table, ctx, kv_heads, head_dim, dtype, which):
+    """[ctx, kv_heads, head_dim] float64 of a sequence's K or V, by torch indexing."""
+    arr = (pool.k if which == "k" else pool.v)[layer].view(np.uint16).reshape(pool.num_blocks, pool.block_size,
+                                                                             kv_heads, head_dim)
+    t = torch.from_numpy(arr.view(np.int16)).view(torch.float16 if dtype == "fp16" else torch.bfloat16).double()
+    tok = torch.arange(ctx)
+    return t[torch.from_numpy(table.astype(np.int64))[tok // pool.block_size], tok % pool.block_size]
+
+
+def _as_f64(bits, dtype):
+    t = torch.from_numpy(np.ascontiguousarray(bits).view(np.int16))
+    return t.view(torch.float16 if dtype == "fp16" else torch.bfloat16).double()
+
+
+def pin_attention_matches_torch(orc):
+    rng = np.random.default_rng(31)
+    for dtype, group, ctx in (("fp16", 1, [5, 16, 33, 1]), ("bf16", 4, [40, 7]), ("fp16", 2, [64, 0, 3])):
+        L, nb, bs, hkv, d = 2, 40, 8, 2, 16
+        pool, q, tables = _attn_case(rng, L, nb, bs, hkv, d, group, ctx, dtype)
+        scale = 1 / np.sqrt(d)
+        got = orc.decode_attention(pool, hkv, d, dtype, q, tables, ctx, scale)
+        qf = _as_f64(q, dtype)
+        for l in range(L):
+            for b, c in enumerate(ctx):
+                if c == 0:
+                    assert not got[l, b].any()
+                    continue
+                K = _dense(pool, l, tables[b], c, hkv, d, dtype, "k").repeat_interleave(group, dim=1)
+                V = _dense(pool, l, tables[b], c, hkv, d, dtype, "v").repeat_interleave(group, dim=1)
+                s = torch.einsum("hd,thd->ht", qf[l, b], K) * scale
+                want = torch.einsum("ht,thd->hd", torch.softmax(s, dim=1), V).numpy()
+                assert np.allclose(got[l, b], want, rtol=1e-12, atol=1e-12), (dtype, l, b)
+
+
+def pin_attention_special_cases(orc):
+    rng = np.random.default_rng(37)
+    L, nb, bs, hkv, d, group = 1, 12, 4, 2, 8, 3
+    # one token: the output is that token's V row
+    pool, q, tables = _attn_case(rng, L, nb, bs, hkv, d, group, [1], "fp16")
+    got = orc.decode_attention(pool, hkv, d, "fp16", q, tables, [1], 0.7)
+    V = _dense(pool, 0, tables[0], 1, hkv, d, "fp16", "v")[0].repeat_interleave(group, dim=0).numpy()
+    assert np.array_equal(got[0, 0], V)
+    # zero scale: uniform weights, the output is the mean of V
+    pool, q, tables = _attn_case(rng, L, nb, bs, hkv, d, group, [11], "bf16")
+    got = orc.decode_attention(pool, hkv, d, "bf16", q, tables, [11], 0.0)
+    V = _dense(pool, 0, tables[0], 11, hkv, d, "bf16", "v").repeat_interleave(group, dim=1).mean(0).numpy()
+    assert np.allclose(got[0, 0], V, rtol=1e-13, atol=1e-13)
+    # grouped heads: V non-zero in KV head 1 only -> query heads of group 1 alone see it
+    for a in pool.v:
+        a.view(np.uint16).reshape(nb, bs, hkv, d)[:, :, 0, :] = 0
+    got = orc.decode_attention(pool, hkv, d, "bf16", q, tables, [11], 0.5)
+    assert not got[0, 0, :group].any() and np.abs(got[0, 0, group:]).max() > 0
+
+
+def pin_attention_token_order_invariant(orc):
+    """Attention is a sum over tokens: permuting where tokens live (blocks
+    and slots) together with the table leaves the output unchanged."""
+    rng = np.random.default_rng(41)
+    L, nb, bs, hkv, d, group, ctx = 1, 16, 4, 1, 8, 2, 16
+    pool, q, tables = _attn_case(rng, L, nb, bs, hkv, d, group, [ctx], "fp16")
+    base = orc.decode_attention(pool, hkv, d, "fp16", q, tables, [ctx], 0.3)
+    # shuffle the four blocks of the table, moving their contents along
+    perm = rng.permutation(4)
+    moved = pool.copy()
+    new_table = tables.copy()
+    spare = [x for x in range(nb) if x not in set(tables[0].tolist())][:4]
+    for j in range(4):
+        src_blk, dst_blk = tables[0, perm[j]], spare[j]
+        for arr_new, arr_old in zip(moved.k + moved.v, pool.k + pool.v):
+            arr_new[dst_blk] = arr_old[src_blk]
+        new_table[0, j] = dst_blk
+    # new logical block j holds old block perm[j]: token order changes, the set does not
+    got = orc.decode_attention(moved, hkv, d, "fp16", q, new_table, [ctx], 0.3)
+    assert np.allclose(got, base, rtol=1e-12, atol=1e-12)
 
 
 ALL_PINS = [v for k, v in sorted(globals().items()) if k.startswith("pin_")]

@@ -44,6 +44,15 @@ MUTANTS = [
      "if (0)", 0),
     ("mismatch_skips_last_token", "for (int64_t t = 0; t < len; t++) {\n        for (int32_t l = 0;",
      "for (int64_t t = 0; t < len - 1; t++) {\n        for (int32_t l = 0;", 0),
+    ("attn_head_map", "int32_t g = h / group;", "int32_t g = h % kv_heads;", 0),
+    ("attn_no_scale", "                    s *= scale;\n", "", 0),
+    ("attn_denominator_counts", "denom += w;", "denom += 1.0;", 0),
+    ("attn_drops_last_token", "for (int32_t t = 0; t < ctx[b]; t++) {\n                    int64_t row",
+     "for (int32_t t = 0; t < ctx[b] - 1; t++) {\n                    int64_t row", 1),
+    ("attn_v_from_k", "o[d] += w * elem(pool_v[l]", "o[d] += w * elem(pool_k[l]", 0),
+    ("half_exponent_bias", "exp - 25", "exp - 24", 0),
+    ("half_subnormal_scale", "ldexp((double)frac, -24)", "ldexp((double)frac, -25)", 0),
+    ("attn_row_slot", "+ t % block_size) * kv_heads + g;", "+ t % block_size) * kv_heads;", 0),
 ]
 
 RUNNER = r"""
