@@ -262,6 +262,29 @@ int llmig_migration_info(const llmig_migration *m, int32_t *state, int64_t *copi
 int llmig_stream_read(const void *region, int64_t bytes, int32_t passes, int32_t workgroups,
                       uint64_t *out, int64_t out_words, void *stream);
 
+/* Decode attention over a pool: the per-step KV reads of the requests that
+ * keep decoding on an instance while one of them migrates (§6.2 measures
+ * their decode speed during migration).  For every layer l, sequence b and
+ * query head h (KV head g = h / (q_heads / num_kv_heads)):
+ *     out[l][b][h][:] = sum_t p_t V_l[t][g][:],
+ *     p = softmax_t(scale * q[l][b][h][:] . K_l[t][g][:]), t < ctx_lens[b],
+ * token t of sequence b living in slot t % block_size of block
+ * tables[b * table_stride + t / block_size].  q is device memory
+ * [num_layers][batch][q_heads][head_dim] of the pool's 16-bit type (dtype 0
+ * fp16, 1 bf16), 16-byte aligned; tables device int32, ids the caller
+ * guarantees in range; ctx_lens a HOST array; out device float32
+ * [num_layers][batch][q_heads][head_dim]; a sequence of length 0 gives
+ * zeros.  workspace: device memory of at least the size
+ * llmig_decode_attention_workspace returns for the same lengths.
+ * Supported: head_dim 64 or 128, q_heads / num_kv_heads in {1, 2, 4, 8},
+ * batch <= 256; else LLMIG_EINVAL.  Arithmetic in fp32. */
+int llmig_decode_attention_workspace(const int32_t *ctx_lens, int32_t batch, int32_t num_layers,
+                                     int32_t q_heads, int32_t head_dim, int64_t *bytes);
+int llmig_decode_attention(const llmig_pool *pool, int32_t dtype, const void *q, int32_t batch,
+                           int32_t q_heads, const int32_t *tables, int32_t table_stride,
+                           const int32_t *ctx_lens, float scale, void *workspace,
+                           int64_t workspace_bytes, float *out, void *stream);
+
 /* Static description of a code; never NULL. */
 const char *llmig_strerror(int code);
 

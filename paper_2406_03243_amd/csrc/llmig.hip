@@ -5,8 +5,10 @@
 // of §5; the interface comments in llmig.h state what every call computes.
 //
 // Sources: common.h (shared kernel definitions), copy_tiles.h (the tile
-// copy and its launch configuration), this file (pool registry, planner,
-// coordinator, harness kernels, argument checks and the C ABI).
+// copy and its launch configuration), decode_attention.h (paged decode
+// attention, the work measured beside a migration), this file (pool
+// registry, planner, coordinator, harness kernels, argument checks and the
+// C ABI).
 
 #include <hip/hip_runtime.h>
 
@@ -20,6 +22,7 @@
 #include "llmig.h"
 #include "common.h"
 #include "copy_tiles.h"
+#include "decode_attention.h"
 
 struct llmig_pool {
     int32_t num_layers, num_blocks, block_size, num_kv_heads, head_dim, elem_bytes;
@@ -636,6 +639,113 @@ int llmig_stream_read(const void *region, int64_t bytes, int32_t passes, int32_t
     void *args[] = {&r, &words, &np, &out};
     hipError_t e = hipLaunchKernel(reinterpret_cast<const void *>(&stream_read_words), dim3(workgroups),
                                    dim3(kThreads), args, 0, static_cast<hipStream_t>(stream));
+    return e == hipSuccess ? LLMIG_OK : hip_error(e);
+}
+
+// Work items of a decode-attention call: one per partition of each sequence.
+static int attn_items(const int32_t *ctx_lens, int32_t batch, std::vector<int32_t> &seq,
+                      std::vector<int32_t> &start, std::vector<int32_t> &end)
+{
+    for (int32_t b = 0; b < batch; ++b) {
+        if (ctx_lens[b] < 0)
+            return LLMIG_EINVAL;
+        for (int32_t t = 0; t < ctx_lens[b]; t += kPartTokens) {
+            seq.push_back(b);
+            start.push_back(t);
+            end.push_back(std::min(ctx_lens[b], t + kPartTokens));
+        }
+    }
+    return LLMIG_OK;
+}
+
+int llmig_decode_attention_workspace(const int32_t *ctx_lens, int32_t batch, int32_t num_layers, int32_t q_heads,
+                                     int32_t head_dim, int64_t *bytes)
+{
+    if (!bytes)
+        return LLMIG_EINVAL;
+    *bytes = 0;
+    if (!ctx_lens || batch < 1 || batch > kAttnMaxBatch || num_layers < 1 || q_heads < 1 || head_dim < 1)
+        return LLMIG_EINVAL;
+    std::vector<int32_t> seq, start, end;
+    if (attn_items(ctx_lens, batch, seq, start, end) != LLMIG_OK)
+        return LLMIG_EINVAL;
+    *bytes = static_cast<int64_t>(num_layers) * static_cast<int64_t>(seq.size()) * q_heads * (head_dim + 2) * 4;
+    return LLMIG_OK;
+}
+
+int llmig_decode_attention(const llmig_pool *pool, int32_t dtype, const void *q, int32_t batch, int32_t q_heads,
+                           const int32_t *tables, int32_t table_stride, const int32_t *ctx_lens, float scale,
+                           void *workspace, int64_t workspace_bytes, float *out, void *stream)
+{
+    if (!pool || (dtype != 0 && dtype != 1) || pool->elem_bytes != 2 || !q || !tables || !ctx_lens || !out ||
+        batch < 1 || batch > kAttnMaxBatch || q_heads < 1 || table_stride < 1)
+        return LLMIG_EINVAL;
+    const int32_t D = pool->head_dim, hkv = pool->num_kv_heads;
+    if (q_heads % hkv != 0)
+        return LLMIG_EINVAL;
+    const void *fn = attn_kernel_for(dtype, D, q_heads / hkv);
+    if (!fn || (reinterpret_cast<uintptr_t>(q) & 15u) || (reinterpret_cast<uintptr_t>(out) & 3u) ||
+        (reinterpret_cast<uintptr_t>(tables) & 3u) || (reinterpret_cast<uintptr_t>(workspace) & 3u))
+        return LLMIG_EINVAL;
+    for (int32_t b = 0; b < batch; ++b)
+        if (ctx_lens[b] < 0 || (ctx_lens[b] + pool->block_size - 1) / pool->block_size > table_stride)
+            return LLMIG_EINVAL;
+    std::vector<int32_t> seq, start, end;
+    if (attn_items(ctx_lens, batch, seq, start, end) != LLMIG_OK)
+        return LLMIG_EINVAL;
+    const int64_t n_items = static_cast<int64_t>(seq.size());
+    const int64_t need = static_cast<int64_t>(pool->num_layers) * n_items * q_heads * (D + 2) * 4;
+    if (n_items > 0 && (!workspace || workspace_bytes < need))
+        return LLMIG_EINVAL;
+    hipStream_t st = static_cast<hipStream_t>(stream);
+
+    AttnArgs a;
+    std::memset(&a, 0, sizeof(a));
+    a.k_tab = pool->d_tab;
+    a.q = static_cast<const uint8_t *>(q);
+    a.tables = tables;
+    a.ws = static_cast<float *>(workspace);
+    a.scale = scale;
+    a.num_layers = static_cast<uint32_t>(pool->num_layers);
+    a.batch = static_cast<uint32_t>(batch);
+    a.q_heads = static_cast<uint32_t>(q_heads);
+    a.kv_heads = static_cast<uint32_t>(hkv);
+    a.block_size = static_cast<uint32_t>(pool->block_size);
+    a.table_stride = static_cast<uint32_t>(table_stride);
+    a.n_items_total = static_cast<uint32_t>(n_items);
+    for (int64_t first = 0; first < n_items; first += kAttnItems) {
+        const int64_t m = std::min<int64_t>(kAttnItems, n_items - first);
+        a.item_base = static_cast<uint32_t>(first);
+        a.items = static_cast<uint32_t>(m);
+        std::memcpy(a.item_seq, seq.data() + first, m * sizeof(int32_t));
+        std::memcpy(a.item_start, start.data() + first, m * sizeof(int32_t));
+        std::memcpy(a.item_end, end.data() + first, m * sizeof(int32_t));
+        void *args[] = {&a};
+        hipError_t e = hipLaunchKernel(fn, dim3(static_cast<uint32_t>(m * hkv), a.num_layers), dim3(kThreads), args,
+                                       0, st);
+        if (e != hipSuccess)
+            return hip_error(e);
+    }
+    AttnReduceArgs r;
+    std::memset(&r, 0, sizeof(r));
+    r.ws = static_cast<const float *>(workspace);
+    r.out = out;
+    r.num_layers = a.num_layers;
+    r.batch = a.batch;
+    r.q_heads = a.q_heads;
+    r.head_dim = static_cast<uint32_t>(D);
+    r.n_items_total = a.n_items_total;
+    for (int64_t i = 0, b = 0; b < batch; ++b) {
+        r.seq_first[b] = static_cast<int32_t>(i);
+        while (i < n_items && seq[i] == b)
+            ++i;
+        r.seq_count[b] = static_cast<int32_t>(i) - r.seq_first[b];
+    }
+    const uint64_t total = static_cast<uint64_t>(pool->num_layers) * batch * q_heads * D;
+    const uint32_t grid = static_cast<uint32_t>(std::min<uint64_t>((total + kThreads - 1) / kThreads, 1u << 20));
+    void *rargs[] = {&r};
+    hipError_t e = hipLaunchKernel(reinterpret_cast<const void *>(&attn_reduce), dim3(grid), dim3(kThreads), rargs, 0,
+                                   st);
     return e == hipSuccess ? LLMIG_OK : hip_error(e);
 }
 

@@ -83,6 +83,12 @@ _lib.llmig_migration_set_max_workgroups.argtypes = [_vp, ctypes.c_int32]
 _lib.llmig_migration_set_max_workgroups.restype = ctypes.c_int
 _lib.llmig_migration_info.argtypes = [_vp, ctypes.POINTER(ctypes.c_int32), _i64p, _i64p, _i64p]
 _lib.llmig_migration_info.restype = ctypes.c_int
+_lib.llmig_decode_attention_workspace.argtypes = [_vp, ctypes.c_int32, ctypes.c_int32, ctypes.c_int32,
+                                                  ctypes.c_int32, _i64p]
+_lib.llmig_decode_attention_workspace.restype = ctypes.c_int
+_lib.llmig_decode_attention.argtypes = [_vp, ctypes.c_int32, _vp, ctypes.c_int32, ctypes.c_int32, _vp,
+                                        ctypes.c_int32, _vp, ctypes.c_float, _vp, ctypes.c_int64, _vp, _vp]
+_lib.llmig_decode_attention.restype = ctypes.c_int
 _lib.llmig_strerror.argtypes = [ctypes.c_int]
 _lib.llmig_strerror.restype = ctypes.c_char_p
 _lib.llmig_last_hip_error.argtypes = []
@@ -303,6 +309,33 @@ class MigrationHandle:
     def commit(self) -> np.ndarray:
         """Commit after the final stage; returns the destination block table."""
         return self._take(_lib.llmig_migration_commit, "llmig_migration_commit")
+
+
+def decode_workspace_bytes(ctx_lens, num_layers: int, q_heads: int, head_dim: int) -> int:
+    c = _host_i32(ctx_lens)
+    n = ctypes.c_int64(0)
+    _check(_lib.llmig_decode_attention_workspace(c.ctypes.data, c.size, int(num_layers), int(q_heads),
+                                                 int(head_dim), ctypes.byref(n)), "llmig_decode_attention_workspace")
+    return n.value
+
+
+def llmig_decode_attention(pool: Pool, q: torch.Tensor, tables: torch.Tensor, ctx_lens, scale: float,
+                           workspace: torch.Tensor, out: torch.Tensor, stream=None) -> None:
+    """Decode attention over ``pool`` (the work beside a migration).  q: CUDA
+    [L][B][Hq][D] fp16/bf16; tables: CUDA int32 [B][stride]; ctx_lens: host
+    lengths; out: CUDA float32 [L][B][Hq][D]."""
+    if q.dtype not in (torch.float16, torch.bfloat16) or not q.is_cuda or not q.is_contiguous():
+        raise ValueError("q must be a contiguous CUDA fp16/bf16 tensor")
+    if tables.dtype != torch.int32 or not tables.is_cuda or not tables.is_contiguous() or tables.dim() != 2:
+        raise ValueError("tables must be a contiguous CUDA int32 [batch][stride] tensor")
+    if out.dtype != torch.float32 or not out.is_cuda or not out.is_contiguous() or out.shape != q.shape:
+        raise ValueError("out must be a contiguous CUDA float32 tensor shaped like q")
+    c = _host_i32(ctx_lens)
+    _check(_lib.llmig_decode_attention(pool.handle, 1 if q.dtype == torch.bfloat16 else 0, q.data_ptr(),
+                                       q.shape[1], q.shape[2], tables.data_ptr(), tables.shape[1],
+                                       c.ctypes.data, float(scale), workspace.data_ptr(),
+                                       workspace.numel() * workspace.element_size(), out.data_ptr(),
+                                       _stream(stream)), "llmig_decode_attention")
 
 
 def llmig_stream_read(region: torch.Tensor, passes: int, workgroups: int, out: torch.Tensor, stream=None) -> None:
