@@ -5,20 +5,15 @@
 // For layer l, sequence b and query head h (KV head g = h / group):
 //     out[l][b][h] = softmax_t(scale * q[l][b][h] . K_l[t][g]) . V_l[t][g]
 // over the sequence's ctx tokens, reached through its block table; inputs
-// are fp16 or bf16, arithmetic and output fp32.
+// are fp16 or bf16, accumulation and output fp32.
 //
-// Design (decode is HBM-bound: each K/V byte feeds `group` multiply-adds):
-//  * split sequences into partitions of kPartTokens tokens (flash-decoding)
-//    so a long request does not leave one workgroup working alone; a work
-//    item is (layer, partition of a sequence, KV head);
-//  * a row of head_dim elements is read by head_dim / 8 lanes with one
-//    16-byte load each, so a 256-lane workgroup covers 256 / (head_dim / 8)
-//    tokens per step with fully coalesced loads;
-//  * the `group` query heads sharing the KV head live in registers; every
-//    lane keeps an online softmax (running max, sum and weighted V) per head
-//    for the tokens it sees, merged across lanes by shuffles and across the
-//    four wavefronts through LDS;
-//  * a second kernel merges the partitions of each sequence.
+// Layout of the work: sequences are cut into partitions of kPartTokens
+// tokens (flash-decoding), so a long request does not leave one workgroup
+// working alone; a workgroup takes one (layer, partition, KV head) and its
+// four wavefronts take alternate 16-token groups of the partition; a second
+// kernel merges the partitions of each sequence.  With `group` query heads
+// per KV head, every K/V byte feeds `group` multiply-adds, a small dense
+// contraction that runs on the matrix cores (see attn_partial_mfma).
 #pragma once
 
 #include "common.h"
@@ -43,163 +38,6 @@ struct AttnArgs {
     int32_t item_start[kAttnItems];
     int32_t item_end[kAttnItems];
 };
-
-template <int BF16>
-__device__ __forceinline__ float to_float(uint32_t bits16)
-{
-    if (BF16)
-        return __builtin_bit_cast(float, bits16 << 16);
-    return static_cast<float>(__builtin_bit_cast(_Float16, static_cast<uint16_t>(bits16)));
-}
-
-template <int BF16>
-__device__ __forceinline__ void unpack8(u32x4 w, float (&x)[8])
-{
-    const uint32_t v[4] = {w.x, w.y, w.z, w.w};
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-        x[2 * i] = to_float<BF16>(v[i] & 0xffffu);
-        x[2 * i + 1] = to_float<BF16>(v[i] >> 16);
-    }
-}
-
-// Merge online-softmax state (m2, l2, a2) into (m, l, a).
-__device__ __forceinline__ void merge_state(float &m, float &l, float (&a)[8], float m2, float l2,
-                                            const float (&a2)[8])
-{
-    const float mm = fmaxf(m, m2);
-    if (mm == -INFINITY)
-        return;
-    const float c1 = __expf(m - mm), c2 = __expf(m2 - mm);
-    l = l * c1 + l2 * c2;
-#pragma unroll
-    for (int i = 0; i < 8; ++i)
-        a[i] = a[i] * c1 + a2[i] * c2;
-    m = mm;
-}
-
-template <int BF16, int D, int G>
-__global__ void __launch_bounds__(kThreads) attn_partial(const AttnArgs a)
-{
-    constexpr int LPT = D / 8;               // lanes per token row
-    constexpr int TPI = kThreads / LPT;      // tokens per step
-    __shared__ float sh_m[4][G], sh_l[4][G], sh_a[4][G][D];
-
-    const uint32_t item = blockIdx.x / a.kv_heads;
-    const uint32_t g = blockIdx.x - item * a.kv_heads;
-    const uint32_t layer = blockIdx.y;
-    const uint32_t b = static_cast<uint32_t>(a.item_seq[item]);
-    const int32_t start = a.item_start[item], end = a.item_end[item];
-    const uint32_t lane_tok = threadIdx.x / LPT;
-    const uint32_t dslice = (threadIdx.x % LPT) * 8;
-
-    const uint8_t *kbase = reinterpret_cast<const uint8_t *>(table_entry(a.k_tab, layer));
-    const uint8_t *vbase = reinterpret_cast<const uint8_t *>(table_entry(a.k_tab, a.num_layers + layer));
-
-    float q[G][8];
-#pragma unroll
-    for (int j = 0; j < G; ++j) {
-        const uint64_t qoff = ((static_cast<uint64_t>(layer) * a.batch + b) * a.q_heads + g * G + j) * D + dslice;
-        unpack8<BF16>(load16(a.q + qoff * 2), q[j]);
-    }
-    float m[G], l[G], acc[G][8];
-#pragma unroll
-    for (int j = 0; j < G; ++j) {
-        m[j] = -INFINITY;
-        l[j] = 0.f;
-#pragma unroll
-        for (int i = 0; i < 8; ++i)
-            acc[j][i] = 0.f;
-    }
-
-    const int32_t *table = a.tables + static_cast<uint64_t>(b) * a.table_stride;
-    for (int32_t t0 = start; t0 < end; t0 += TPI) {
-        const int32_t t = t0 + static_cast<int32_t>(lane_tok);
-        const bool valid = t < end;
-        float k[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
-        float v[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
-        if (valid) {
-            const int32_t blk = table[t / a.block_size];
-            const uint64_t row = (static_cast<uint64_t>(blk) * a.block_size + t % a.block_size) * a.kv_heads + g;
-            unpack8<BF16>(load16(kbase + (row * D + dslice) * 2), k);
-            unpack8<BF16>(load16(vbase + (row * D + dslice) * 2), v);
-        }
-#pragma unroll
-        for (int j = 0; j < G; ++j) {
-            float s = 0.f;
-#pragma unroll
-            for (int i = 0; i < 8; ++i)
-                s += q[j][i] * k[i];
-#pragma unroll
-            for (int off = LPT / 2; off > 0; off /= 2)
-                s += __shfl_xor(s, off);
-            if (valid) {
-                s *= a.scale;
-                const float mm = fmaxf(m[j], s);
-                const float c = __expf(m[j] - mm), e = __expf(s - mm);
-                l[j] = l[j] * c + e;
-#pragma unroll
-                for (int i = 0; i < 8; ++i)
-                    acc[j][i] = acc[j][i] * c + e * v[i];
-                m[j] = mm;
-            }
-        }
-    }
-
-    // merge the token rows of a wavefront: lanes with the same dslice
-#pragma unroll
-    for (int j = 0; j < G; ++j) {
-#pragma unroll
-        for (int off = LPT; off < 64; off *= 2) {
-            float a2[8];
-#pragma unroll
-            for (int i = 0; i < 8; ++i)
-                a2[i] = __shfl_xor(acc[j][i], off);
-            const float m2 = __shfl_xor(m[j], off), l2 = __shfl_xor(l[j], off);
-            merge_state(m[j], l[j], acc[j], m2, l2, a2);
-        }
-    }
-    // merge the four wavefronts through LDS
-    const uint32_t wave = threadIdx.x / 64, wl = threadIdx.x % 64;
-    if (wl < LPT) {
-#pragma unroll
-        for (int j = 0; j < G; ++j) {
-            if (wl == 0) {
-                sh_m[wave][j] = m[j];
-                sh_l[wave][j] = l[j];
-            }
-#pragma unroll
-            for (int i = 0; i < 8; ++i)
-                sh_a[wave][j][dslice + i] = acc[j][i];
-        }
-    }
-    __syncthreads();
-    if (threadIdx.x < static_cast<uint32_t>(LPT)) {
-        const uint64_t slot = (static_cast<uint64_t>(layer) * a.n_items_total + a.item_base + item) * a.q_heads;
-#pragma unroll
-        for (int j = 0; j < G; ++j) {
-            float mm = sh_m[0][j], ll = sh_l[0][j], aa[8];
-#pragma unroll
-            for (int i = 0; i < 8; ++i)
-                aa[i] = sh_a[0][j][dslice + i];
-            for (int w = 1; w < 4; ++w) {
-                float a2[8];
-#pragma unroll
-                for (int i = 0; i < 8; ++i)
-                    a2[i] = sh_a[w][j][dslice + i];
-                merge_state(mm, ll, aa, sh_m[w][j], sh_l[w][j], a2);
-            }
-            float *dst = a.ws + (slot + g * G + j) * (D + 2);
-#pragma unroll
-            for (int i = 0; i < 8; ++i)
-                dst[2 + dslice + i] = aa[i];
-            if (threadIdx.x == 0) {
-                dst[0] = mm;
-                dst[1] = ll;
-            }
-        }
-    }
-}
 
 struct AttnReduceArgs {
     const float *ws;
@@ -239,21 +77,253 @@ __global__ void __launch_bounds__(kThreads) attn_reduce(const AttnReduceArgs a)
     }
 }
 
+// ---------------------------------------------------------------------------
+// Matrix-core variant.  Per 16-token group of a partition, one wavefront:
+//   S^T = K . Q^T     16 tokens x 16 query rows (the group's heads, zero-padded),
+//                     K fragments loaded straight from HBM, 16 bytes a lane,
+//                     16x16x32 MFMA over head_dim in steps of 32;
+//   online softmax per query row (a lane's rows of S^T are the tokens
+//                     4*(lane/16) .. +3 of query row lane%16);
+//   O^T += V^T . P^T  16x16x16 MFMA per 16 dims; P^T is already in the
+//                     B-operand layout, V^T goes through LDS (the layout
+//                     transposes there).  P is split into a 16-bit high part
+//                     and the 16-bit rounding of the remainder, two MFMAs, so
+//                     the weights keep ~2^-16 (bf16) / 2^-22 (fp16) precision.
+// The four wavefronts take alternate token groups of the partition and merge
+// their states through LDS at the end.
+typedef _Float16 f16x8_t __attribute__((ext_vector_type(8)));
+typedef _Float16 f16x4_t __attribute__((ext_vector_type(4)));
+typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
+typedef short i16x4_t __attribute__((ext_vector_type(4)));
+typedef float f32x4_t __attribute__((ext_vector_type(4)));
+
+template <int BF16>
+__device__ __forceinline__ f32x4_t mfma_qk(u32x4 a, u32x4 b, f32x4_t c)
+{
+    if constexpr (BF16)
+        return __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, a),
+                                                        __builtin_bit_cast(bf16x8_t, b), c, 0, 0, 0);
+    else
+        return __builtin_amdgcn_mfma_f32_16x16x32_f16(__builtin_bit_cast(f16x8_t, a),
+                                                       __builtin_bit_cast(f16x8_t, b), c, 0, 0, 0);
+}
+
+template <int BF16>
+__device__ __forceinline__ f32x4_t mfma_pv(uint64_t a, uint64_t b, f32x4_t c)
+{
+    if constexpr (BF16)
+        return __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(__builtin_bit_cast(i16x4_t, a),
+                                                          __builtin_bit_cast(i16x4_t, b), c, 0, 0, 0);
+    else
+        return __builtin_amdgcn_mfma_f32_16x16x16f16(__builtin_bit_cast(f16x4_t, a),
+                                                      __builtin_bit_cast(f16x4_t, b), c, 0, 0, 0);
+}
+
+// Round a float to the 16-bit type (nearest even); returns the bits.
+template <int BF16>
+__device__ __forceinline__ uint32_t to16(float x)
+{
+    if constexpr (BF16) {
+        const uint32_t u = __builtin_bit_cast(uint32_t, x);
+        return (u + 0x7fffu + ((u >> 16) & 1u)) >> 16;
+    } else {
+        return __builtin_bit_cast(uint16_t, static_cast<_Float16>(x));
+    }
+}
+
+template <int BF16, int D>
+__global__ void __launch_bounds__(kThreads) attn_partial_mfma(const AttnArgs a)
+{
+    constexpr int KS = D / 32;            // k-steps of the QK product
+    constexpr int MT = D / 16;            // 16-dim tiles of the PV product
+    constexpr int LPR = D / 8;            // lanes per row in the V loads (16 bytes each)
+    constexpr int RPL = 64 / LPR;         // rows per V load instruction
+    constexpr int VP = 20;                // LDS pitch of one V^T row: 16 tokens + 4 pad (40 bytes)
+    constexpr float kLog2e = 1.4426950408889634f;
+    // 4 wavefronts x D rows x VP in the loop; reused for the final merge of
+    // 4 x D x 16 floats.
+    constexpr int kVtBytes = 4 * D * VP * 2, kMergeBytes = 4 * D * 16 * 4;
+    __shared__ __align__(16) uint8_t smem[kVtBytes > kMergeBytes ? kVtBytes : kMergeBytes];
+    __shared__ float sh_m[4][16], sh_l[4][16];
+    __shared__ int32_t sh_blk[kPartTokens];         // block ids of the partition (block_size >= 1)
+
+    const uint32_t item = blockIdx.x / a.kv_heads;
+    const uint32_t g = blockIdx.x - item * a.kv_heads;
+    const uint32_t layer = blockIdx.y;
+    const uint32_t b = static_cast<uint32_t>(a.item_seq[item]);
+    const int32_t start = a.item_start[item], end = a.item_end[item];
+    const uint32_t G = a.q_heads / a.kv_heads;
+    const uint32_t wave = threadIdx.x / 64, lane = threadIdx.x % 64;
+    const uint32_t r16 = lane % 16, g4 = lane / 16;
+
+    const uint8_t *kbase = reinterpret_cast<const uint8_t *>(table_entry(a.k_tab, layer));
+    const uint8_t *vbase = reinterpret_cast<const uint8_t *>(table_entry(a.k_tab, a.num_layers + layer));
+    uint16_t *vt = reinterpret_cast<uint16_t *>(smem) + wave * D * VP;
+
+    // The partition's block ids, once, so no token waits on a table load.
+    const int32_t *table = a.tables + static_cast<uint64_t>(b) * a.table_stride;
+    const int32_t first_blk = start / static_cast<int32_t>(a.block_size);
+    const int32_t n_blk = (end - 1) / static_cast<int32_t>(a.block_size) - first_blk + 1;
+    for (int32_t k = threadIdx.x; k < n_blk; k += kThreads)
+        sh_blk[k] = table[first_blk + k];
+    __syncthreads();
+
+    // Q^T fragments (B operand): query row r16 of the group, dims 32*ks + 8*g4 .. +8.
+    u32x4 qf[KS];
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) {
+        qf[ks] = u32x4{0u, 0u, 0u, 0u};
+        if (r16 < G) {
+            const uint64_t qoff = ((static_cast<uint64_t>(layer) * a.batch + b) * a.q_heads + g * G + r16) * D +
+                                  32 * ks + 8 * g4;
+            qf[ks] = load16(a.q + qoff * 2);
+        }
+    }
+    const float qk_scale = a.scale * kLog2e;
+    float m = -INFINITY, lsum = 0.f;
+    f32x4_t acc[MT];
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt)
+        acc[mt] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+
+    for (int32_t tg = start + 16 * static_cast<int32_t>(wave); tg < end; tg += 64) {
+        // K fragments (A operand): token tg + r16, dims 32*ks + 8*g4 .. +8.
+        const int32_t tk = tg + static_cast<int32_t>(r16);
+        u32x4 kf[KS];
+        if (tk < end) {
+            const uint64_t row = (static_cast<uint64_t>(sh_blk[tk / a.block_size - first_blk]) * a.block_size +
+                                  tk % a.block_size) * a.kv_heads + g;
+#pragma unroll
+            for (int ks = 0; ks < KS; ++ks)
+                kf[ks] = load16(kbase + (row * D + 32 * ks + 8 * g4) * 2);
+        } else {
+#pragma unroll
+            for (int ks = 0; ks < KS; ++ks)
+                kf[ks] = u32x4{0u, 0u, 0u, 0u};
+        }
+        // V rows: KS loads of RPL rows x D dims; row tg + j*RPL + lane/LPR, dims 8*(lane%LPR) .. +8.
+        u32x4 vr[KS];
+#pragma unroll
+        for (int j = 0; j < KS; ++j) {
+            const int32_t tv = tg + j * RPL + static_cast<int32_t>(lane / LPR);
+            vr[j] = u32x4{0u, 0u, 0u, 0u};
+            if (tv < end) {
+                const uint64_t row = (static_cast<uint64_t>(sh_blk[tv / a.block_size - first_blk]) *
+                                      a.block_size + tv % a.block_size) * a.kv_heads + g;
+                vr[j] = load16(vbase + (row * D + 8 * (lane % LPR)) * 2);
+            }
+        }
+        // S^T = K . Q^T
+        f32x4_t s = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks)
+            s = mfma_qk<BF16>(kf[ks], qf[ks], s);
+        // V^T into LDS: element (token, dim) at vt[dim * VP + token - tg]
+#pragma unroll
+        for (int j = 0; j < KS; ++j) {
+            const uint32_t tok = j * RPL + lane / LPR, d0 = 8 * (lane % LPR);
+            const uint32_t w4[4] = {vr[j].x, vr[j].y, vr[j].z, vr[j].w};
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                vt[(d0 + 2 * e) * VP + tok] = static_cast<uint16_t>(w4[e] & 0xffffu);
+                vt[(d0 + 2 * e + 1) * VP + tok] = static_cast<uint16_t>(w4[e] >> 16);
+            }
+        }
+        // online softmax for query row r16 over tokens tg + 4*g4 + i
+        float sc[4], mx = -INFINITY;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            sc[i] = tg + static_cast<int32_t>(4 * g4) + i < end ? s[i] * qk_scale : -INFINITY;
+            mx = fmaxf(mx, sc[i]);
+        }
+        mx = fmaxf(mx, __shfl_xor(mx, 16));
+        mx = fmaxf(mx, __shfl_xor(mx, 32));
+        const float m_new = fmaxf(m, mx);          // finite: the group has a valid token
+        const float c = exp2f(m - m_new);
+        float p[4], ps = 0.f;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            p[i] = exp2f(sc[i] - m_new);
+            ps += p[i];
+        }
+        ps += __shfl_xor(ps, 16);
+        ps += __shfl_xor(ps, 32);
+        lsum = lsum * c + ps;
+        m = m_new;
+        uint64_t ph = 0, pl = 0;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            const uint32_t hi = to16<BF16>(p[i]);
+            const float hv = BF16 ? __builtin_bit_cast(float, hi << 16)
+                                  : static_cast<float>(__builtin_bit_cast(_Float16, static_cast<uint16_t>(hi)));
+            ph |= static_cast<uint64_t>(hi) << (16 * i);
+            pl |= static_cast<uint64_t>(to16<BF16>(p[i] - hv)) << (16 * i);
+        }
+        // the wavefront's own LDS writes above precede its reads below
+        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+        __builtin_amdgcn_wave_barrier();
+        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+#pragma unroll
+        for (int mt = 0; mt < MT; ++mt) {
+            const uint64_t vf = *reinterpret_cast<const uint64_t *>(vt + (16 * mt + r16) * VP + 4 * g4);
+            acc[mt] = acc[mt] * c;
+            acc[mt] = mfma_pv<BF16>(vf, ph, acc[mt]);
+            acc[mt] = mfma_pv<BF16>(vf, pl, acc[mt]);
+        }
+        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+        __builtin_amdgcn_wave_barrier();
+        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+    }
+
+    // merge the four wavefronts: state of query row r16, O^T rows 16*mt + 4*g4 + i
+    __syncthreads();                                // every wave is done with its V^T region
+    float *so = reinterpret_cast<float *>(smem);    // [wave][dim][16]
+    if (g4 == 0) {
+        sh_m[wave][r16] = m;
+        sh_l[wave][r16] = lsum;
+    }
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+            so[(wave * D + 16 * mt + 4 * g4 + i) * 16 + r16] = acc[mt][i];
+    __syncthreads();
+    if (wave == 0 && r16 < G) {
+        float mm = -INFINITY;
+        for (int w = 0; w < 4; ++w)
+            mm = fmaxf(mm, sh_m[w][r16]);
+        float cw[4], ll = 0.f;
+        for (int w = 0; w < 4; ++w) {
+            cw[w] = mm == -INFINITY ? 0.f : exp2f(sh_m[w][r16] - mm);
+            ll += sh_l[w][r16] * cw[w];
+        }
+        const uint64_t slot = (static_cast<uint64_t>(layer) * a.n_items_total + a.item_base + item) * a.q_heads +
+                              g * G + r16;
+        float *dst = a.ws + slot * (D + 2);
+#pragma unroll
+        for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                const uint32_t dim = 16 * mt + 4 * g4 + i;
+                float o = 0.f;
+                for (int w = 0; w < 4; ++w)
+                    o += so[(w * D + dim) * 16 + r16] * cw[w];
+                dst[2 + dim] = o;
+            }
+        if (g4 == 0) {
+            // the reduce kernel merges with natural exponentials: store m in that base
+            dst[0] = mm == -INFINITY ? -INFINITY : mm / kLog2e;
+            dst[1] = ll;
+        }
+    }
+}
+
 template <int BF16, int D>
 const void *attn_kernel(int group)
 {
-    switch (group) {
-    case 1:
-        return reinterpret_cast<const void *>(&attn_partial<BF16, D, 1>);
-    case 2:
-        return reinterpret_cast<const void *>(&attn_partial<BF16, D, 2>);
-    case 4:
-        return reinterpret_cast<const void *>(&attn_partial<BF16, D, 4>);
-    case 8:
-        return reinterpret_cast<const void *>(&attn_partial<BF16, D, 8>);
-    default:
-        return nullptr;
-    }
+    if (group >= 1 && group <= 16 && (group & (group - 1)) == 0)
+        return reinterpret_cast<const void *>(&attn_partial_mfma<BF16, D>);
+    return nullptr;
 }
 
 const void *attn_kernel_for(int bf16, int head_dim, int group)

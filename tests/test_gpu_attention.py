@@ -2,7 +2,10 @@
 migration) against the fp64 oracle, through the C ABI.
 
 Tolerance: inputs are exact fp16/bf16 values in [-1, 1]; the kernel
-multiplies and accumulates in fp32 and uses the hardware exp2.  A softmax-
+multiplies them on the matrix cores with fp32 accumulation, exponentiates in
+fp32, and carries the softmax weights into the P.V product as a 16-bit high
+part plus the 16-bit rounding of the rest (about 2^-16 relative for bf16,
+2^-22 for fp16).  A softmax-
 weighted mean of values in [-1, 1] accumulated over n tokens in fp32 is off
 by at most about n * eps32 = n * 6e-8, so a case whose longest sequence has
 n tokens allows an absolute error of max(1e-4, n * 6e-8) plus 1e-4
@@ -69,6 +72,8 @@ CASES = [
     (1, 400, 16, 2, 128, 4, [4096, 5, 2000], "bf16"),
     (3, 100, 8, 1, 64, 2, [96, 95, 97, 1], "fp16"),
     (1, 2000, 16, 1, 128, 2, [30000, 29999, 20000], "fp16"),  # 158 partitions: two launches of items
+    (2, 120, 16, 1, 128, 16, [700, 33], "bf16"),               # 16 query heads on one KV head
+    (1, 300, 4, 2, 64, 4, [1000, 3, 62], "bf16"),             # 4-token blocks: a 16-token group spans blocks
 ]
 
 
