@@ -405,6 +405,7 @@ def load_section(reps=3, reader_passes=3, step_ms=20.0, caps=(0, 256, 64)):
     out = {"workload": su.workload.name, "tokens": length, "reader_bytes": read_bytes,
            "reader_workgroups": wgs, "reader_alone_GBps": round(read_bytes / (r_alone * 1e-6) / 1e9, 1),
            "by_cap": {}}
+    out["beside_decode"] = decode_overhead(su, caps, step_ms)
     for cap in caps:
         alone_m = []
         for r in range(reps + 1):
@@ -439,6 +440,74 @@ def load_section(reps=3, reader_passes=3, step_ms=20.0, caps=(0, 256, 64)):
             "downtime_us_under_load": round(statistics.median(b[2] for b in both), 1)}
     su.close()
     return out
+
+
+def decode_overhead(su, caps, step_ms, steps=14, reps=5):
+    """Per-step decode attention time on the source instance (a batch of
+    16 requests plus the migrating one, all 80 layers) with and without a
+    migration running beside it (Llumnix §6.2 reports at most 1% slowdown)."""
+    import torch
+
+    from paper_2406_03243_amd import migrate, scenarios
+    from paper_2406_03243_amd.llmig import decode_workspace_bytes, llmig_decode_attention
+
+    shape, src, dst, table, free = su.shape, su.src, su.dst, su.tables[0], su.free
+    append_pool = su.extra["append_pool"]
+    tables, ctx, q = scenarios.decode_batch(su)
+    out = torch.empty(q.shape, dtype=torch.float32, device="cuda")
+    ws = torch.empty(decode_workspace_bytes(ctx, shape.num_layers, q.shape[2], shape.head_dim),
+                     dtype=torch.uint8, device="cuda")
+    scale = 1.0 / math.sqrt(shape.head_dim)
+    at, mig, dec = torch.cuda.Stream(), torch.cuda.Stream(), torch.cuda.Stream()
+    kv_bytes = sum(ctx) * shape.num_layers * 2 * shape.kv_heads * shape.head_dim * shape.elem_bytes
+
+    def decode_steps(n):
+        evs = [torch.cuda.Event(enable_timing=True) for _ in range(n + 1)]
+        evs[0].record(at)
+        for i in range(n):
+            llmig_decode_attention(src, q, tables, ctx, scale, ws, out, stream=at)
+            evs[i + 1].record(at)
+        return evs
+
+    for _ in range(3):
+        llmig_decode_attention(src, q, tables, ctx, scale, ws, out, stream=at)
+    torch.cuda.synchronize()
+    evs = decode_steps(steps)
+    torch.cuda.synchronize()
+    alone = [evs[i].elapsed_time(evs[i + 1]) * 1e3 for i in range(steps)]
+    t_alone = statistics.median(alone)
+    res = {"batch": len(ctx), "tokens": int(sum(ctx)), "kv_bytes_per_step": kv_bytes,
+           "step_us_alone": round(t_alone, 1), "decode_GBps_alone": round(kv_bytes / (t_alone * 1e-6) / 1e9, 1),
+           "by_cap": {}}
+    for cap in caps:
+        rows = []
+        for r in range(reps):
+            torch.cuda.synchronize()
+            evs = decode_steps(steps)
+            m0 = torch.cuda.Event(enable_timing=True)
+            m1 = torch.cuda.Event(enable_timing=True)
+            # let two decode steps run, then start the migration beside them
+            mig.wait_event(evs[2])
+            m0.record(mig)
+            m, dt = migrate.run_timed(src, dst, table, su.lengths[0], free, append_pool, mig, dec,
+                                      step_ms=step_ms, max_workgroups=cap)
+            m1.record(mig)
+            torch.cuda.synchronize()
+            start, stop = evs[0].elapsed_time(m0), evs[0].elapsed_time(m1)
+            over = [evs[i].elapsed_time(evs[i + 1]) * 1e3 for i in range(steps)
+                    if evs[0].elapsed_time(evs[i + 1]) > start and evs[0].elapsed_time(evs[i]) < stop]
+            rows.append((over, (stop - start) * 1e3, dt))
+        over = [x for o, _, _ in rows for x in o]
+        res["by_cap"][str(cap) if cap else "uncapped"] = {
+            "migration_us": round(statistics.median(r[1] for r in rows), 1),
+            "overlapping_steps": round(statistics.mean(len(r[0]) for r in rows), 1),
+            "extra_decode_us_per_migration": round(statistics.median(sum(x - t_alone for x in r[0])
+                                                                     for r in rows), 1),
+            "step_us_during_migration_mean": round(statistics.mean(over), 1),
+            "step_us_during_migration_max": round(max(over), 1),
+            "decode_slowdown_during_migration": round(statistics.mean(over) / t_alone - 1, 3),
+            "downtime_us": round(statistics.median(r[2] for r in rows), 1)}
+    return res
 
 
 if __name__ == "__main__":

@@ -120,3 +120,27 @@ def gqa_long(dev="cuda", max_append=256) -> Setup:
     harness.fill_on_device([region], w.seed * 16 + wl.EXTRA)
     return Setup(w, w.shape, src, dst, [table], [w.lengths[0]], free, socc, docc,
                  extra={"append_pool": pool.to(dev), "region": region})
+
+
+def decode_batch(su: Setup, n_seq: int = 16, q_heads: int = 64, seed_purpose: int = wl.EXTRA, dev="cuda"):
+    """A decode batch on the source instance of a GQA setup: ``n_seq``
+    requests filling the blocks the migrating request does not use (equal
+    shares, random order) plus the migrating request itself with its initial
+    length.  Returns (tables [B][stride] int32 device tensor, context
+    lengths, q [L][B][q_heads][D] device tensor)."""
+    shape, table = su.shape, su.tables[0]
+    rest = np.setdiff1d(np.arange(shape.num_blocks, dtype=np.int32), table)
+    g = wl.stream(su.workload.seed, seed_purpose, 11)
+    rest = g.permutation(rest)
+    per = len(rest) // n_seq
+    stride = max(per, len(table))
+    tabs = np.zeros((n_seq + 1, stride), np.int32)
+    for k in range(n_seq):
+        tabs[k, :per] = rest[k * per:(k + 1) * per]
+    tabs[n_seq, :len(table)] = table
+    ctx = [per * shape.block_size] * n_seq + [su.lengths[0]]
+    bits = wl.values16(su.workload.seed, seed_purpose, shape.num_layers * (n_seq + 1) * q_heads * shape.head_dim,
+                       shape.dtype, sub=12)
+    q = torch.from_numpy(bits.view(np.int16)).view(harness.TORCH_DTYPE[shape.dtype]).reshape(
+        shape.num_layers, n_seq + 1, q_heads, shape.head_dim)
+    return torch.from_numpy(tabs).to(dev), ctx, q.to(dev)
