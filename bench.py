@@ -63,6 +63,17 @@ def recorded_traffic(kernel: str):
     return rec["traffic_bytes_per_launch"]
 
 
+def bulk_span_rows(tile_bytes: int) -> int:
+    """The copy kernel's span (1 KiB rows per wavefront) for a bulk launch:
+    the power of two at or above a quarter of the tile, within [2, 32]
+    (mirrors the library's launch configuration, for labelling only)."""
+    quarter = -(-tile_bytes // 4096)
+    span = 2
+    while span < 32 and span < quarter:
+        span *= 2
+    return span
+
+
 def stage_bytes(blocks, shape, tile_bytes):
     """Algorithmic bytes of a stage: every tile read once and written once."""
     return 2 * blocks * shape.num_layers * 2 * tile_bytes
@@ -156,7 +167,7 @@ def main():
     per_launch_us = s1_avg_us / launches
     achieved = per_launch_bytes / (per_launch_us * 1e-6) / 1e9
     downtimes = [d for _, d in runs]
-    kernel_name = "copy_tiles<0, 0, true, %d>" % (16 if src.tile_bytes >= 32 * 4096 else 8)
+    kernel_name = "copy_tiles<0, 0, true, %d>" % bulk_span_rows(src.tile_bytes)
 
     stages = []
     for i, rec in enumerate(m0.stages):

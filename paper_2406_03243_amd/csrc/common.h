@@ -12,11 +12,7 @@
 namespace {
 
 constexpr int kThreads = 256;                 // 4 wavefronts of 64 lanes
-constexpr uint32_t kRowBytes = kThreads * 16; // one 16-byte word per lane
-constexpr int kBulkRows = 8;                  // rows per item of a bulk copy: 32 KiB in flight
-constexpr int kWideRows = 16;                 // rows per item of a bulk copy of tiles >= 32 rows
-constexpr int kSmallRows = 2;                 // rows per item of a small (latency-bound) copy
-constexpr uint32_t kBulkItemsPerCU = 16;      // a launch with fewer items than this per CU is small
+constexpr uint32_t kRowBytes = kThreads * 16; // one 16-byte word per lane of a workgroup
 constexpr int kInlinePairs = 256;             // ids carried in the kernel arguments per launch
 
 typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));

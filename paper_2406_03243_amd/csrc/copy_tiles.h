@@ -10,13 +10,18 @@
 // Kernel design (CDNA4, wave64):
 //  * The work of a call is a list of tiles, one per (pair, layer, K/V); a
 //    tile is tile_bytes contiguous bytes on both sides.  A tile is cut into
-//    rows of 4 KiB (256 lanes x 16 B), and a workgroup item is a chunk of up
-//    to ROWS rows of one tile: each lane issues all of its 16-byte loads
-//    (global_load_dwordx4) before its first store, so every lane keeps
-//    ROWS x 16 B in flight and each wavefront instruction moves 1 KiB of
-//    contiguous, fully coalesced memory.  Bulk copies use 8- or 16-row
-//    chunks; small copies (a final stage) use 2-row chunks to spread over
-//    more CUs.
+//    SPAN-KiB spans and each span is one wavefront's work item: the wave
+//    issues SPAN 1-KiB loads (64 lanes x 16 bytes, global_load_dwordx4)
+//    before its first store, so each lane keeps SPAN x 16 bytes in flight
+//    and the wave streams one contiguous span in and out.  SPAN is about a
+//    quarter of the tile, so the four wavefronts of a workgroup move one
+//    whole tile: measured on MI355X, long per-wave spans beat interleaving
+//    the wavefronts over shared 4 KiB rows by 5-16% (128 KiB tiles: 32 KiB
+//    spans, 6.1-6.3 against 5.3-5.4 TB/s).  Launches with few items (a
+//    final stage) use 2 KiB spans so their tiles spread over more CUs.
+//  * Wave items run pair-major (all spans of all layers of one block pair,
+//    then the next pair); one workgroup per four items unless the grid is
+//    capped, in which case resident workgroups walk the items.
 //  * The block ids of an item are wavefront-uniform; they and the per-layer
 //    base addresses are read with scalar loads, so the only vector memory
 //    traffic is the copy itself.
@@ -29,8 +34,6 @@
 //  * Loads and stores are non-temporal: every byte is touched once, and
 //    streaming it past the caches leaves them to the decode work running
 //    beside the migration (measured 2-4% faster than cached accesses).
-//  * Items run pair-major (all layers of one block pair, then the next
-//    pair), one workgroup per item.
 #pragma once
 
 #include <algorithm>
@@ -56,26 +59,25 @@ struct CopyArgs {
     uint32_t num_layers;
     uint32_t planes;            // 2 * num_layers
     uint32_t pairs;             // pairs in this launch
-    uint32_t chunks_per_tile;
-    uint32_t rows_per_chunk;    // <= ROWS of the kernel
-    uint32_t items;             // pairs * 2 * num_layers * chunks_per_tile
+    uint32_t spans_per_tile;
+    uint32_t items;             // wave items: pairs * planes * spans_per_tile
     uint32_t lin_first;         // this launch's first pair within the whole call
     uint32_t lin_pairs;         // pairs in the whole call
     int32_t src_ids[kInlinePairs];
     int32_t dst_ids[kInlinePairs];
 };
 
-template <int SRC, int DST, bool INLINE_IDS, int ROWS>
+constexpr uint32_t kWaveRow = 64 * 16;         // one wavefront load: 1 KiB
+
+template <int SRC, int DST, bool INLINE_IDS, int SPAN>
 __global__ void __launch_bounds__(kThreads) copy_tiles(const CopyArgs a)
 {
-    const uint32_t lane_off = threadIdx.x * 16u;
-    const uint32_t full_rows = a.tile_bytes / kRowBytes; // complete 4 KiB rows of a tile
-    for (uint32_t item = blockIdx.x; item < a.items; item += gridDim.x) {
-        // Items run pair-major: consecutive workgroups take the chunks of one
-        // block pair across all layers and K/V, so the memory they touch at
-        // a time is spread over many layer tensors.
-        const uint32_t tile = item / a.chunks_per_tile;
-        const uint32_t chunk = item - tile * a.chunks_per_tile;
+    const uint32_t lane_off = (threadIdx.x % 64) * 16u;
+    const uint32_t waves = gridDim.x * (kThreads / 64);
+    for (uint32_t w = blockIdx.x * (kThreads / 64) + threadIdx.x / 64; w < a.items; w += waves) {
+        const uint32_t item = uniform(w);
+        const uint32_t tile = item / a.spans_per_tile;
+        const uint32_t span = item - tile * a.spans_per_tile;
         const uint32_t i = tile / a.planes;
         const uint32_t plane = tile - i * a.planes; // layer * 2 + kv
         const uint32_t layer = plane >> 1, kv = plane & 1u;
@@ -97,45 +99,28 @@ __global__ void __launch_bounds__(kThreads) copy_tiles(const CopyArgs a)
             d = a.dst_lin + (static_cast<uint64_t>(plane) * a.lin_pairs + a.lin_first + i) * a.tile_bytes;
         }
 
-        const uint32_t row0 = chunk * a.rows_per_chunk;
-        const uint32_t first = row0 * kRowBytes + lane_off;
-        // Rows of this chunk that every lane copies whole (wavefront-uniform).
-        const uint32_t whole = full_rows > row0 ? min(a.rows_per_chunk, full_rows - row0) : 0u;
-        u32x4 r[ROWS];
-        if (whole == ROWS) {
-            // Common case: ROWS complete rows, no predication at all.
+        const uint32_t first = span * SPAN * kWaveRow + lane_off;
+        u32x4 r[SPAN];
+        if ((span + 1) * SPAN * kWaveRow <= a.tile_bytes) {
+            // Common case: a whole span, no predication at all.
 #pragma unroll
-            for (int u = 0; u < ROWS; ++u)
-                r[u] = load16(s + first + u * kRowBytes);
+            for (int u = 0; u < SPAN; ++u)
+                r[u] = load16(s + first + u * kWaveRow);
 #pragma unroll
-            for (int u = 0; u < ROWS; ++u)
-                store16(d + first + u * kRowBytes, r[u]);
+            for (int u = 0; u < SPAN; ++u)
+                store16(d + first + u * kWaveRow, r[u]);
         } else {
-            // Fewer rows: uniform branches for the whole rows, a lane
-            // predicate only for a final partial row of the tile.
+            // The tile's last span is short: a lane predicate per 1 KiB row.
 #pragma unroll
-            for (int u = 0; u < ROWS; ++u)
-                if (u < static_cast<int>(whole))
-                    r[u] = load16(s + first + u * kRowBytes);
+            for (int u = 0; u < SPAN; ++u)
+                if (first + u * kWaveRow < a.tile_bytes)
+                    r[u] = load16(s + first + u * kWaveRow);
 #pragma unroll
-            for (int u = 0; u < ROWS; ++u)
-                if (u < static_cast<int>(whole))
-                    store16(d + first + u * kRowBytes, r[u]);
-            const uint32_t tail = first + whole * kRowBytes;
-            if (whole < a.rows_per_chunk && row0 + whole == full_rows && tail < a.tile_bytes)
-                store16(d + tail, load16(s + tail));
+            for (int u = 0; u < SPAN; ++u)
+                if (first + u * kWaveRow < a.tile_bytes)
+                    store16(d + first + u * kWaveRow, r[u]);
         }
     }
-}
-
-// Row split of one tile: rows of kRowBytes, chunks of at most max_rows
-// rows, balanced so every chunk of a tile carries nearly the same number.
-void split_tile(uint32_t tile_bytes, uint32_t max_rows, uint32_t *chunks, uint32_t *rows_per_chunk)
-{
-    const uint32_t rows = (tile_bytes + kRowBytes - 1) / kRowBytes;
-    const uint32_t c = (rows + max_rows - 1) / max_rows;
-    *chunks = c;
-    *rows_per_chunk = (rows + c - 1) / c;
 }
 
 uint32_t compute_units()
@@ -150,32 +135,42 @@ uint32_t compute_units()
     return cus;
 }
 
-// One workgroup per item: measured on MI355X, letting the dispatcher hand
-// out items beats a resident grid walking them (the loop in the kernels
-// stays, so a capped grid remains correct).
-uint32_t grid_for(uint32_t items)
+// Span (in 1 KiB rows) for a bulk copy: the power of two nearest above a
+// quarter of the tile, between 2 and 32.
+int bulk_span(uint32_t tile_bytes)
 {
-    return items;
+    const uint32_t quarter = (tile_bytes + 4 * kWaveRow - 1) / (4 * kWaveRow);
+    int span = 2;
+    while (span < 32 && static_cast<uint32_t>(span) < quarter)
+        span *= 2;
+    return span;
 }
 
 template <int SRC, int DST, bool INLINE_IDS>
-const void *copy_kernel_rows(int rows)
+const void *copy_kernel_span(int span)
 {
-    switch (rows) {
-    case kWideRows:
-        return reinterpret_cast<const void *>(&copy_tiles<SRC, DST, INLINE_IDS, kWideRows>);
-    case kBulkRows:
-        return reinterpret_cast<const void *>(&copy_tiles<SRC, DST, INLINE_IDS, kBulkRows>);
+    switch (span) {
+    case 32:
+        return reinterpret_cast<const void *>(&copy_tiles<SRC, DST, INLINE_IDS, 32>);
+    case 16:
+        return reinterpret_cast<const void *>(&copy_tiles<SRC, DST, INLINE_IDS, 16>);
+    case 8:
+        return reinterpret_cast<const void *>(&copy_tiles<SRC, DST, INLINE_IDS, 8>);
+    case 4:
+        return reinterpret_cast<const void *>(&copy_tiles<SRC, DST, INLINE_IDS, 4>);
     default:
-        return reinterpret_cast<const void *>(&copy_tiles<SRC, DST, INLINE_IDS, kSmallRows>);
+        return reinterpret_cast<const void *>(&copy_tiles<SRC, DST, INLINE_IDS, 2>);
     }
 }
 
 template <int SRC, int DST>
-const void *copy_kernel(bool ids_on_device, int rows)
+const void *copy_kernel(bool ids_on_device, int span)
 {
-    return ids_on_device ? copy_kernel_rows<SRC, DST, false>(rows) : copy_kernel_rows<SRC, DST, true>(rows);
+    return ids_on_device ? copy_kernel_span<SRC, DST, false>(span) : copy_kernel_span<SRC, DST, true>(span);
 }
+
+// A launch with fewer wave items than this per CU is small (a final stage).
+constexpr uint32_t kBulkWaveItemsPerCU = 16;
 
 // max_workgroups > 0 caps the grid: fewer, resident workgroups walk the
 // items, leaving the rest of the chip (and of HBM) to other work.
@@ -183,31 +178,22 @@ template <int SRC, int DST>
 int launch_copy(CopyArgs a, const int32_t *src_ids, const int32_t *dst_ids, int64_t n,
                 bool ids_on_device, hipStream_t stream, uint32_t max_workgroups = 0)
 {
-    // Bulk copies take chunks of kBulkRows rows (most bytes in flight per
-    // lane); small ones, such as a final stage, take kSmallRows-row chunks so
-    // their few tiles spread over more CUs and finish sooner.
-    // Tiles of 32 rows or more take 16-row chunks (measured ~1% faster on
-    // 128 KiB tiles than 8-row ones).
-    uint32_t chunks = 0, rpc = 0;
-    const uint32_t tile_rows = (a.tile_bytes + kRowBytes - 1) / kRowBytes;
-    int rows = tile_rows >= 2u * kWideRows ? kWideRows : kBulkRows;
-    split_tile(a.tile_bytes, rows, &chunks, &rpc);
+    int span = bulk_span(a.tile_bytes);
+    uint32_t spt = (a.tile_bytes + span * kWaveRow - 1) / (span * kWaveRow);
     const uint64_t pairs_first_launch =
         std::min<int64_t>(n, ids_on_device ? n : static_cast<int64_t>(kInlinePairs));
-    const bool bulk = pairs_first_launch * 2ull * a.num_layers * chunks >= kBulkItemsPerCU * compute_units();
-    if (!bulk) {
-        rows = kSmallRows;
-        split_tile(a.tile_bytes, rows, &chunks, &rpc);
+    if (pairs_first_launch * 2ull * a.num_layers * spt < kBulkWaveItemsPerCU * compute_units()) {
+        span = 2;
+        spt = (a.tile_bytes + span * kWaveRow - 1) / (span * kWaveRow);
     }
-    a.chunks_per_tile = chunks;
-    a.rows_per_chunk = rpc;
-    const uint64_t items_per_pair = 2ull * a.num_layers * a.chunks_per_tile;
+    a.spans_per_tile = spt;
+    const uint64_t items_per_pair = 2ull * a.num_layers * spt;
     uint64_t per_launch = ids_on_device ? (0x7fffffffull / items_per_pair) : kInlinePairs;
     if (per_launch == 0)
         return LLMIG_EINVAL;
     a.lin_pairs = static_cast<uint32_t>(n);
     a.planes = 2u * a.num_layers;
-    const void *fn = copy_kernel<SRC, DST>(ids_on_device, rows);
+    const void *fn = copy_kernel<SRC, DST>(ids_on_device, span);
     for (int64_t first = 0; first < n; first += static_cast<int64_t>(per_launch)) {
         const uint32_t m = static_cast<uint32_t>(std::min<int64_t>(n - first, per_launch));
         a.pairs = m;
@@ -223,7 +209,7 @@ int launch_copy(CopyArgs a, const int32_t *src_ids, const int32_t *dst_ids, int6
                 std::memcpy(a.dst_ids, dst_ids + first, m * sizeof(int32_t));
         }
         void *args[] = {&a};
-        uint32_t grid = grid_for(a.items);
+        uint32_t grid = (a.items + kThreads / 64 - 1) / (kThreads / 64);
         if (max_workgroups > 0)
             grid = std::min(grid, max_workgroups);
         hipError_t e = hipLaunchKernel(fn, dim3(grid), dim3(kThreads), args, 0, stream);
