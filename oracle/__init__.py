@@ -32,6 +32,12 @@ LIBRARY = os.path.join(HERE, "libllmig_oracle.so")
 OK, EINVAL, ENOSPC, ERANGE = 0, -1, -2, -3
 ERROR_NAMES = {OK: "OK", EINVAL: "EINVAL", ENOSPC: "ENOSPC", ERANGE: "ERANGE"}
 
+# Intra-tile layouts of a (layer, K or V, block) tile of bs tokens, H heads,
+# D dims (x = 16 / elem_bytes): NHD [bs][H][D], HND [H][bs][D],
+# HCNX [H][D/x][bs][x], HDN [H][D][bs].
+NHD, HND, HCNX, HDN = 0, 1, 2, 3
+LAYOUT_NAMES = {NHD: "NHD", HND: "HND", HCNX: "HCNX", HDN: "HDN"}
+
 
 def build(source: str = SOURCE, library: str = LIBRARY, quiet: bool = False) -> str:
     """Compile the C oracle with gcc into a shared library; returns its path."""
@@ -134,6 +140,21 @@ class Oracle:
         lib.oracle_half_to_double.argtypes = [ctypes.c_uint16]
         lib.oracle_bf16_to_double.restype = ctypes.c_double
         lib.oracle_bf16_to_double.argtypes = [ctypes.c_uint16]
+        lib.oracle_layout_offset.restype = ctypes.c_int64
+        lib.oracle_layout_offset.argtypes = [ctypes.c_int32, ctypes.c_int64, ctypes.c_int64, ctypes.c_int64,
+                                             ctypes.c_int32, ctypes.c_int32, ctypes.c_int32, ctypes.c_int32]
+        lib.oracle_copy_layout.restype = None
+        lib.oracle_copy_layout.argtypes = [_pp, _pp, _i32p, _pp, _pp, _i32p, ctypes.c_int32, ctypes.c_int32,
+                                           ctypes.c_int32, ctypes.c_int32, ctypes.c_int32, _i32p, _i32p,
+                                           ctypes.c_int64]
+        lib.oracle_write_tokens_layout.restype = None
+        lib.oracle_write_tokens_layout.argtypes = [_pp, _pp, _i32p, ctypes.c_int32, ctypes.c_int32,
+                                                   ctypes.c_int32, ctypes.c_int32, ctypes.c_int32, _i32p,
+                                                   ctypes.c_int64, ctypes.c_int64, ctypes.c_void_p]
+        lib.oracle_first_token_mismatch_layout.restype = ctypes.c_int64
+        lib.oracle_first_token_mismatch_layout.argtypes = [_pp, _pp, _i32p, _i32p, _pp, _pp, _i32p, _i32p,
+                                                           ctypes.c_int32, ctypes.c_int32, ctypes.c_int32,
+                                                           ctypes.c_int32, ctypes.c_int32, ctypes.c_int64]
         lib.oracle_decode_attention.restype = None
         lib.oracle_decode_attention.argtypes = [_pp, _pp, ctypes.c_int32, ctypes.c_int32, ctypes.c_int32,
                                                 ctypes.c_int32, ctypes.c_int, ctypes.c_void_p, ctypes.c_int32,
@@ -225,6 +246,70 @@ class Oracle:
                                                     tb.ctypes.data_as(_i32p), a.num_layers,
                                                     a.block_size, a.slot_bytes, length)
 
+    # ---- cross-layout migration ----
+    def layout_offset(self, layout: int, t: int, h: int, d: int, block_size: int, heads: int, head_dim: int,
+                      elem_bytes: int) -> int:
+        """Byte offset of element (t, h, d) in a tile of the given layout (-1: no such layout)."""
+        return self.lib.oracle_layout_offset(layout, t, h, d, block_size, heads, head_dim, elem_bytes)
+
+    @staticmethod
+    def _geometry(pool: HostPool, heads: int, head_dim: int, elem_bytes: int) -> None:
+        assert pool.slot_bytes == heads * head_dim * elem_bytes
+
+    def copy_layout(self, src: HostPool, src_layouts, dst: HostPool, dst_layouts, map_src, map_dst,
+                    heads: int, head_dim: int, elem_bytes: int) -> None:
+        """One stage from a pool whose (K, V) tiles use ``src_layouts`` into
+        one whose tiles use ``dst_layouts``: every element moves to the
+        position the destination layout gives it."""
+        ms, md = _i32(map_src), _i32(map_dst)
+        assert len(ms) == len(md) and src.num_layers == dst.num_layers
+        assert src.block_size == dst.block_size
+        self._geometry(src, heads, head_dim, elem_bytes)
+        self._geometry(dst, heads, head_dim, elem_bytes)
+        if len(ms):
+            assert ms.min() >= 0 and ms.max() < src.num_blocks
+            assert md.min() >= 0 and md.max() < dst.num_blocks
+        sl, dl = _i32(src_layouts), _i32(dst_layouts)
+        assert len(sl) == 2 and len(dl) == 2
+        for lay in list(sl) + list(dl):
+            assert self.layout_offset(int(lay), 0, 0, 0, src.block_size, heads, head_dim, elem_bytes) >= 0
+        sk, sv = src._ptrs()
+        dk, dv = dst._ptrs()
+        self.lib.oracle_copy_layout(sk, sv, sl.ctypes.data_as(_i32p), dk, dv, dl.ctypes.data_as(_i32p),
+                                    src.num_layers, src.block_size, heads, head_dim, elem_bytes,
+                                    ms.ctypes.data_as(_i32p), md.ctypes.data_as(_i32p), len(ms))
+
+    def write_tokens_layout(self, pool: HostPool, layouts, table, from_tok: int, data: np.ndarray,
+                            heads: int, head_dim: int, elem_bytes: int) -> None:
+        """As :meth:`write_tokens` (data [L][2][n_tok][H*D*e]) into a pool of the given (K, V) layouts."""
+        self._geometry(pool, heads, head_dim, elem_bytes)
+        t = _i32(table)
+        lay = _i32(layouts)
+        data = np.ascontiguousarray(data, dtype=np.uint8)
+        n_tok = data.size // (pool.num_layers * 2 * pool.slot_bytes)
+        assert data.size == pool.num_layers * 2 * n_tok * pool.slot_bytes and len(lay) == 2
+        if n_tok:
+            assert (from_tok + n_tok - 1) // pool.block_size < len(t)
+        k, v = pool._ptrs()
+        self.lib.oracle_write_tokens_layout(k, v, lay.ctypes.data_as(_i32p), pool.num_layers, pool.block_size,
+                                            heads, head_dim, elem_bytes, t.ctypes.data_as(_i32p), from_tok,
+                                            n_tok, data.ctypes.data)
+
+    def first_token_mismatch_layout(self, a: HostPool, a_layouts, table_a, b: HostPool, b_layouts, table_b,
+                                    length: int, heads: int, head_dim: int, elem_bytes: int) -> int:
+        ta, tb = _i32(table_a), _i32(table_b)
+        la, lb = _i32(a_layouts), _i32(b_layouts)
+        self._geometry(a, heads, head_dim, elem_bytes)
+        self._geometry(b, heads, head_dim, elem_bytes)
+        assert a.block_size == b.block_size
+        if length:
+            assert (length - 1) // a.block_size < min(len(ta), len(tb))
+        ak, av = a._ptrs()
+        bk, bv = b._ptrs()
+        return self.lib.oracle_first_token_mismatch_layout(
+            ak, av, la.ctypes.data_as(_i32p), ta.ctypes.data_as(_i32p), bk, bv, lb.ctypes.data_as(_i32p),
+            tb.ctypes.data_as(_i32p), a.num_layers, a.block_size, heads, head_dim, elem_bytes, length)
+
     # ---- decode attention over the paged pool (the work beside a migration) ----
     def half_to_double(self, bits: int) -> float:
         return self.lib.oracle_half_to_double(bits)
@@ -256,7 +341,7 @@ class Oracle:
         return out
 
     # ---- multi-stage migration (Llumnix §4.2) ----
-    def migrate(self, src: HostPool, dst: HostPool, src_table, dst_free_list, events):
+    def migrate(self, src: HostPool, dst: HostPool, src_table, dst_free_list, events, layouts=None):
         """Replay a migration on host pools.
 
         ``events`` is the ordered list of what happened to the request:
@@ -266,19 +351,29 @@ class Oracle:
         ``length`` tokens were resident.  Each stage takes its destination
         blocks from the head of what is left of the free list.  Returns the
         request's destination block table (one id per logical block, in
-        logical order) and the list of per-stage (map_src, map_dst)."""
+        logical order) and the list of per-stage (map_src, map_dst).
+
+        ``layouts`` = (src_layouts, dst_layouts, heads, head_dim, elem_bytes)
+        replays a cross-layout migration: appends land in the source's
+        layouts and every stage converts into the destination's."""
         free = list(_i32(dst_free_list))
         dst_table = []
         stages = []
         for ev in events:
             if ev[0] == "append":
-                self.write_tokens(src, src_table, ev[1], ev[2])
+                if layouts is None:
+                    self.write_tokens(src, src_table, ev[1], ev[2])
+                else:
+                    self.write_tokens_layout(src, layouts[0], src_table, ev[1], ev[2], *layouts[2:])
             elif ev[0] == "stage":
                 _, length, lo, hi = ev
                 code, ms, md = self.plan(src_table, free, length, lo, hi, src.block_size)
                 if code != OK:
                     raise RuntimeError(f"oracle plan failed: {ERROR_NAMES[code]}")
-                self.copy(src, dst, ms, md)
+                if layouts is None:
+                    self.copy(src, dst, ms, md)
+                else:
+                    self.copy_layout(src, layouts[0], dst, layouts[1], ms, md, *layouts[2:])
                 free = free[len(md):]
                 dst_table.extend(int(x) for x in md)
                 stages.append((ms, md))

@@ -358,3 +358,135 @@ void oracle_decode_attention(uint8_t *const *pool_k, uint8_t *const *pool_v, int
         }
     }
 }
+
+/* ------------------------------------------------------------------------
+ * Cross-layout migration: the source and destination instances keep the
+ * (token, head, dim) elements of a tile in different orders.  The copy is
+ * then no longer a byte copy of tiles but the same elements placed where
+ * the destination's layout puts them; whole tiles still move (a partial
+ * last block carries its unused slots along).  Llumnix migrates between
+ * instances of one engine (§4.2); this generalisation keeps its definition,
+ * element for element.
+ *
+ * Layouts of one tile of bs tokens, H heads, D dims, e-byte elements
+ * (x = 16 / e elements form one 16-byte group of a head's dims):
+ *   ORACLE_LAYOUT_NHD  [bs][H][D]         token-major (the vLLM pool above)
+ *   ORACLE_LAYOUT_HND  [H][bs][D]         head-major
+ *   ORACLE_LAYOUT_HCNX [H][D/x][bs][x]    vLLM paged attention's key cache
+ *   ORACLE_LAYOUT_HDN  [H][D][bs]         vLLM paged attention's value cache
+ * ---------------------------------------------------------------------- */
+#define ORACLE_LAYOUT_NHD 0
+#define ORACLE_LAYOUT_HND 1
+#define ORACLE_LAYOUT_HCNX 2
+#define ORACLE_LAYOUT_HDN 3
+
+/* Byte offset of element (t, h, d) inside a tile, or -1 for an unknown
+ * layout or an element size that does not divide 16 (HCNX only). */
+int64_t oracle_layout_offset(int32_t layout, int64_t t, int64_t h, int64_t d,
+                             int32_t bs, int32_t heads, int32_t head_dim, int32_t elem_bytes)
+{
+    int64_t index;
+    if (layout == ORACLE_LAYOUT_NHD) {
+        index = (t * heads + h) * head_dim + d;
+    } else if (layout == ORACLE_LAYOUT_HND) {
+        index = (h * bs + t) * head_dim + d;
+    } else if (layout == ORACLE_LAYOUT_HCNX) {
+        if (elem_bytes <= 0 || 16 % elem_bytes != 0)
+            return -1;
+        int64_t x = 16 / elem_bytes;
+        int64_t groups = head_dim / x;
+        index = ((h * groups + d / x) * bs + t) * x + d % x;
+    } else if (layout == ORACLE_LAYOUT_HDN) {
+        index = (h * head_dim + d) * bs + t;
+    } else {
+        return -1;
+    }
+    return index * elem_bytes;
+}
+
+/* One stage between pools of different layouts: for every pair (s, d),
+ * every layer and both K and V, every element (t, h, dim) of source tile s
+ * is written to the position the destination layout gives it in tile d.
+ * layouts[0] / layouts[1] are the K / V layouts of each side. */
+void oracle_copy_layout(uint8_t *const *src_k, uint8_t *const *src_v, const int32_t *src_layouts,
+                        uint8_t *const *dst_k, uint8_t *const *dst_v, const int32_t *dst_layouts,
+                        int32_t num_layers, int32_t bs, int32_t heads, int32_t head_dim,
+                        int32_t elem_bytes, const int32_t *map_src, const int32_t *map_dst, int64_t n)
+{
+    int64_t tile_bytes = (int64_t)bs * heads * head_dim * elem_bytes;
+    for (int64_t i = 0; i < n; i++) {
+        for (int32_t l = 0; l < num_layers; l++) {
+            for (int kv = 0; kv < 2; kv++) {
+                const uint8_t *s = (kv == 0 ? src_k : src_v)[l] + (int64_t)map_src[i] * tile_bytes;
+                uint8_t *d = (kv == 0 ? dst_k : dst_v)[l] + (int64_t)map_dst[i] * tile_bytes;
+                for (int64_t t = 0; t < bs; t++)
+                    for (int64_t h = 0; h < heads; h++)
+                        for (int64_t e = 0; e < head_dim; e++)
+                            memcpy(d + oracle_layout_offset(dst_layouts[kv], t, h, e, bs, heads,
+                                                            head_dim, elem_bytes),
+                                   s + oracle_layout_offset(src_layouts[kv], t, h, e, bs, heads,
+                                                            head_dim, elem_bytes),
+                                   (size_t)elem_bytes);
+            }
+        }
+    }
+}
+
+/* Decoding's KV appends into a pool of any layout: data is laid out
+ * [layer][K=0, V=1][token][H][D] (each token's K or V in head, dim order)
+ * and element (h, dim) of token t goes where the pool's layout puts it in
+ * slot t % bs of block table[t / bs]. */
+void oracle_write_tokens_layout(uint8_t *const *pool_k, uint8_t *const *pool_v,
+                                const int32_t *layouts, int32_t num_layers, int32_t bs,
+                                int32_t heads, int32_t head_dim, int32_t elem_bytes,
+                                const int32_t *table, int64_t from_tok, int64_t n_tok,
+                                const uint8_t *data)
+{
+    int64_t tile_bytes = (int64_t)bs * heads * head_dim * elem_bytes;
+    for (int32_t l = 0; l < num_layers; l++) {
+        for (int kv = 0; kv < 2; kv++) {
+            uint8_t *const *pool = (kv == 0) ? pool_k : pool_v;
+            for (int64_t j = 0; j < n_tok; j++) {
+                int64_t t = from_tok + j;
+                uint8_t *tile = pool[l] + (int64_t)table[t / bs] * tile_bytes;
+                const uint8_t *src = data + (((int64_t)l * 2 + kv) * n_tok + j) * heads * head_dim * elem_bytes;
+                for (int64_t h = 0; h < heads; h++)
+                    for (int64_t e = 0; e < head_dim; e++)
+                        memcpy(tile + oracle_layout_offset(layouts[kv], t % bs, h, e, bs, heads,
+                                                           head_dim, elem_bytes),
+                               src + (h * head_dim + e) * elem_bytes, (size_t)elem_bytes);
+            }
+        }
+    }
+}
+
+/* Token identity across layouts: -1 when every element (t < len, every
+ * layer, K and V, every head and dim) read through table_a and a's layouts
+ * equals the one read through table_b and b's layouts; else the first token
+ * that differs. */
+int64_t oracle_first_token_mismatch_layout(uint8_t *const *a_k, uint8_t *const *a_v,
+                                           const int32_t *a_layouts, const int32_t *table_a,
+                                           uint8_t *const *b_k, uint8_t *const *b_v,
+                                           const int32_t *b_layouts, const int32_t *table_b,
+                                           int32_t num_layers, int32_t bs, int32_t heads,
+                                           int32_t head_dim, int32_t elem_bytes, int64_t len)
+{
+    int64_t tile_bytes = (int64_t)bs * heads * head_dim * elem_bytes;
+    for (int64_t t = 0; t < len; t++) {
+        for (int32_t l = 0; l < num_layers; l++) {
+            for (int kv = 0; kv < 2; kv++) {
+                const uint8_t *ta = (kv == 0 ? a_k : a_v)[l] + (int64_t)table_a[t / bs] * tile_bytes;
+                const uint8_t *tb = (kv == 0 ? b_k : b_v)[l] + (int64_t)table_b[t / bs] * tile_bytes;
+                for (int64_t h = 0; h < heads; h++)
+                    for (int64_t e = 0; e < head_dim; e++)
+                        if (memcmp(ta + oracle_layout_offset(a_layouts[kv], t % bs, h, e, bs, heads,
+                                                             head_dim, elem_bytes),
+                                   tb + oracle_layout_offset(b_layouts[kv], t % bs, h, e, bs, heads,
+                                                             head_dim, elem_bytes),
+                                   (size_t)elem_bytes) != 0)
+                            return t;
+            }
+        }
+    }
+    return -1;
+}

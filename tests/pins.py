@@ -29,6 +29,12 @@ What pins what:
                gathered sequence; one token gives its V row; zero scale
                gives the mean of V; grouped heads read their own KV head;
                moving the tokens between blocks leaves the output unchanged.
+  * layouts  - every layout's placement equals numpy's reshape/transpose of
+               the [block_size, heads, head_dim] tile, for 1-, 2- and 4-byte
+               elements; offsets are a bijection onto the tile; conversions
+               round-trip and compose; same-layout conversion is the byte
+               copy; appends and token identity read through numpy's view;
+               a cross-layout multi-stage replay keeps every token.
 """
 from __future__ import annotations
 
@@ -38,7 +44,7 @@ import os
 import numpy as np
 import torch
 
-from oracle import EINVAL, ENOSPC, ERANGE, OK, HostPool, stage_bounds
+from oracle import EINVAL, ENOSPC, ERANGE, HCNX, HDN, HND, NHD, OK, HostPool, stage_bounds
 
 GOLDEN = os.path.join(os.path.dirname(os.path.abspath(__file__)), "golden", "paper_worked_examples.json")
 
@@ -456,4 +462,194 @@ def pin_attention_token_order_invariant(orc):
     assert np.allclose(got, base, rtol=1e-12, atol=1e-12)
 
 
-ALL_PINS = [v for k, v in sorted(globals().items()) if k.startswith("pin_")]
+# --------------------------------------------------------------------------- cross-layout
+LAYOUTS = (NHD, HND, HCNX, HDN)
+_UINT = {1: np.uint8, 2: np.uint16, 4: np.uint32}
+
+
+def _arrange(logical, layout, e):
+    """Byte image of a [bs, H, D] tile in ``layout``, by numpy reshape/transpose."""
+    bs, heads, dim = logical.shape
+    if layout == NHD:
+        a = logical
+    elif layout == HND:
+        a = logical.transpose(1, 0, 2)
+    elif layout == HCNX:
+        x = 16 // e
+        a = logical.reshape(bs, heads, dim // x, x).transpose(1, 2, 0, 3)
+    else:
+        a = logical.transpose(1, 2, 0)
+    return np.ascontiguousarray(a).view(np.uint8).reshape(-1)
+
+
+def _logical(tile, layout, bs, heads, dim, e):
+    """[bs, H, D] view of a tile's bytes in ``layout``: the inverse of _arrange."""
+    a = np.ascontiguousarray(tile).view(_UINT[e])
+    if layout == NHD:
+        return a.reshape(bs, heads, dim)
+    if layout == HND:
+        return a.reshape(heads, bs, dim).transpose(1, 0, 2)
+    if layout == HCNX:
+        x = 16 // e
+        return a.reshape(heads, dim // x, bs, x).transpose(2, 0, 1, 3).reshape(bs, heads, dim)
+    return a.reshape(heads, dim, bs).transpose(2, 0, 1)
+
+
+XGEOMS = [(8, 3, 16, 2), (3, 2, 32, 1), (4, 2, 8, 4), (16, 1, 24, 2)]   # bs, heads, head_dim, elem_bytes
+
+
+def pin_xlayout_offsets_bijective(orc):
+    for bs, heads, dim, e in XGEOMS:
+        tile = bs * heads * dim * e
+        for lay in LAYOUTS:
+            offs = sorted(orc.layout_offset(lay, t, h, d, bs, heads, dim, e)
+                          for t in range(bs) for h in range(heads) for d in range(dim))
+            assert offs == list(range(0, tile, e)), (lay, bs, heads, dim, e)
+    assert orc.layout_offset(4, 0, 0, 0, 8, 1, 16, 2) == -1
+    assert orc.layout_offset(HCNX, 0, 0, 0, 8, 1, 16, 3) == -1
+
+
+def pin_xlayout_matches_numpy_transposes(orc):
+    for bs, heads, dim, e in XGEOMS:
+        n_el = bs * heads * dim
+        assert n_el < 256 ** e
+        a_k = (np.arange(n_el) % 256 ** e).astype(_UINT[e]).reshape(bs, heads, dim)
+        a_v = a_k[::-1].copy()
+        slot = heads * dim * e
+        rng = np.random.default_rng(bs * 1000 + dim)
+        for lk in LAYOUTS:
+            for lv in LAYOUTS:
+                src = _random_pool(rng, 2, 3, bs, slot)
+                src.k[1][0] = a_k.view(np.uint8).reshape(-1)
+                src.v[1][0] = a_v.view(np.uint8).reshape(-1)
+                dst = _random_pool(rng, 2, 4, bs, slot)
+                orc.copy_layout(src, (NHD, NHD), dst, (lk, lv), [0], [3], heads, dim, e)
+                assert np.array_equal(dst.k[1][3], _arrange(a_k, lk, e)), (bs, dim, e, lk)
+                assert np.array_equal(dst.v[1][3], _arrange(a_v, lv, e)), (bs, dim, e, lv)
+                back = _random_pool(rng, 2, 2, bs, slot)
+                orc.copy_layout(dst, (lk, lv), back, (NHD, NHD), [3], [1], heads, dim, e)
+                assert np.array_equal(back.k[1][1], src.k[1][0]) and np.array_equal(back.v[1][1], src.v[1][0])
+
+
+def pin_xlayout_round_trip_and_composition(orc):
+    rng = np.random.default_rng(37)
+    bs, heads, dim, e, num_layers = 8, 2, 16, 2, 2
+    slot = heads * dim * e
+    src = _random_pool(rng, num_layers, 6, bs, slot)
+    ms = np.array([4, 0, 5], np.int32)
+    md = np.array([1, 6, 3], np.int32)
+    pairs = [(a, b) for a in LAYOUTS for b in LAYOUTS]
+    for x in pairs:
+        # same layouts on both sides: exactly the byte copy
+        d1, d2 = _random_pool(rng, num_layers, 7, bs, slot), None
+        d2 = d1.copy()
+        orc.copy_layout(src, x, d1, x, ms, md, heads, dim, e)
+        orc.copy(src, d2, ms, md)
+        assert d1.equals(d2), x
+        for y in pairs[(x[0] * 5 + x[1]) % 4::3]:
+            mid = _random_pool(rng, num_layers, 7, bs, slot)
+            orc.copy_layout(src, x, mid, y, ms, md, heads, dim, e)
+            back = src.copy()
+            orc.copy_layout(mid, y, back, x, md, ms, heads, dim, e)
+            assert back.equals(src), (x, y)
+            for z in (pairs[(y[1] * 3 + x[0]) % len(pairs)],):
+                via = _random_pool(rng, num_layers, 8, bs, slot)
+                direct = via.copy()
+                orc.copy_layout(mid, y, via, z, md, [7, 2, 0], heads, dim, e)
+                orc.copy_layout(src, x, direct, z, ms, [7, 2, 0], heads, dim, e)
+                assert via.equals(direct), (x, y, z)
+
+
+def pin_xlayout_appends_and_identity(orc):
+    rng = np.random.default_rng(41)
+    bs, heads, dim, e, num_layers, nb = 8, 3, 16, 2, 2, 9
+    slot = heads * dim * e
+    table = rng.choice(nb, 4, replace=False).astype(np.int32)
+    lo, n_tok = 3, 21
+    data = rng.integers(0, 256, (num_layers, 2, n_tok, slot), dtype=np.uint8)
+    base = _random_pool(rng, num_layers, nb, bs, slot)
+    a, b = base.copy(), base.copy()
+    orc.write_tokens_layout(a, (NHD, NHD), table, lo, data, heads, dim, e)
+    orc.write_tokens(b, table, lo, data)
+    assert a.equals(b)
+    for lay in ((HDN, HCNX), (HND, HDN), (HCNX, NHD)):
+        p = base.copy()
+        orc.write_tokens_layout(p, lay, table, lo, data, heads, dim, e)
+        for l in range(num_layers):
+            for kv, arr in enumerate((p.k[l], p.v[l])):
+                for j in range(n_tok):
+                    t = lo + j
+                    view = _logical(arr[table[t // bs]], lay[kv], bs, heads, dim, e)
+                    want = data[l, kv, j].view(np.uint16).reshape(heads, dim)
+                    assert np.array_equal(view[t % bs], want), (lay, l, kv, t)
+        # slots outside [lo, lo + n_tok) are untouched
+        for l in range(num_layers):
+            for kv, (x, y) in enumerate(((p.k[l], base.k[l]), (p.v[l], base.v[l]))):
+                for blk in range(nb):
+                    vx = _logical(x[blk], lay[kv], bs, heads, dim, e)
+                    vy = _logical(y[blk], lay[kv], bs, heads, dim, e)
+                    for s in range(bs):
+                        hit = blk in table and lo <= list(table).index(blk) * bs + s < lo + n_tok
+                        if not hit:
+                            assert np.array_equal(vx[s], vy[s])
+    # token identity across layouts finds a planted element at its token
+    length = 29
+    src = _random_pool(rng, num_layers, nb, bs, slot)
+    dst = _random_pool(rng, num_layers, nb + 2, bs, slot)
+    tb = rng.choice(nb + 2, 4, replace=False).astype(np.int32)
+    sl, dl = (HND, HDN), (HCNX, NHD)
+    orc.copy_layout(src, sl, dst, dl, table, tb, heads, dim, e)
+    assert orc.first_token_mismatch_layout(src, sl, table, dst, dl, tb, length, heads, dim, e) == -1
+    for t, l, kv, h, d in ((0, 0, 0, 0, 0), (28, 1, 1, 2, 15), (17, 1, 0, 1, 9), (9, 0, 1, 2, 3)):
+        c = dst.copy()
+        arr = (c.k if kv == 0 else c.v)[l][tb[t // bs]]
+        logical = _logical(arr, dl[kv], bs, heads, dim, e).copy()
+        logical[t % bs, h, d] ^= 0x0100
+        arr[:] = _arrange(logical, dl[kv], e)
+        assert orc.first_token_mismatch_layout(src, sl, table, c, dl, tb, length, heads, dim, e) == t
+    c = dst.copy()
+    arr = c.k[0][tb[3]]
+    logical = _logical(arr, dl[0], bs, heads, dim, e).copy()
+    logical[5, 0, 0] ^= 1                                   # token 29: beyond the length
+    arr[:] = _arrange(logical, dl[0], e)
+    assert orc.first_token_mismatch_layout(src, sl, table, c, dl, tb, length, heads, dim, e) == -1
+
+
+def pin_xlayout_multistage_replay(orc):
+    rng = np.random.default_rng(43)
+    bs, heads, dim, e, num_layers = 8, 2, 16, 2, 2
+    slot = heads * dim * e
+    initial, appended = 19, [5, 11, 2]
+    final_len = initial + sum(appended)
+    nb = _ceil_div(final_len, bs)
+    for sl, dl in (((NHD, NHD), (HCNX, HDN)), ((HCNX, HDN), (NHD, NHD)), ((HND, HDN), (HDN, HND))):
+        src = _random_pool(rng, num_layers, 20, bs, slot)
+        dst = _random_pool(rng, num_layers, 22, bs, slot)
+        dst0 = dst.copy()
+        table = rng.choice(20, nb, replace=False).astype(np.int32)
+        free = rng.permutation(22).astype(np.int32)
+        events, cur = [], initial
+        for k, (length, lo, hi) in enumerate(stage_bounds(initial, appended, bs)):
+            if k > 0:
+                data = rng.integers(0, 256, (num_layers, 2, appended[k - 1], slot), dtype=np.uint8)
+                events.append(("append", cur, data))
+                cur += appended[k - 1]
+            events.append(("stage", length, lo, hi))
+        dst_table, _ = orc.migrate(src, dst, table, free, events, layouts=(sl, dl, heads, dim, e))
+        assert np.array_equal(dst_table, free[:nb])
+        for l in range(num_layers):
+            for kv in range(2):
+                sarr = (src.k if kv == 0 else src.v)[l]
+                darr = (dst.k if kv == 0 else dst.v)[l]
+                for j in range(nb):
+                    a = _logical(sarr[table[j]], sl[kv], bs, heads, dim, e)
+                    b = _logical(darr[dst_table[j]], dl[kv], bs, heads, dim, e)
+                    assert np.array_equal(a, b), (sl, dl, l, kv, j)
+        rest = np.setdiff1d(np.arange(22), dst_table)
+        for x, y in zip(dst.k + dst.v, dst0.k + dst0.v):
+            assert np.array_equal(x[rest], y[rest])
+
+
+# In file order: cheap checks of a part run before the pins that would write
+# through a broken part of it.
+ALL_PINS = [v for k, v in globals().items() if k.startswith("pin_")]
