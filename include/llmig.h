@@ -20,10 +20,12 @@
  * [num_blocks, block_size, num_kv_heads, head_dim], each element elem_bytes
  * wide.  One (layer, K or V, block) tile is
  *     tile_bytes = block_size * num_kv_heads * head_dim * elem_bytes
- * contiguous bytes (128 KB for 16 tokens of 16-bit LLaMA-7B, §5).  The copy
- * moves whole tiles as raw bytes and never converts them, so any 16-bit
- * format (fp16, bf16) and any bit pattern (NaN payloads, -0, subnormals)
- * arrives unchanged.
+ * contiguous bytes (128 KB for 16 tokens of 16-bit LLaMA-7B, §5).  Between
+ * pools of one layout the copy moves whole tiles as raw bytes and never
+ * converts them, so any element format (fp16, bf16) and any bit pattern
+ * (NaN payloads, -0, subnormals) arrives unchanged; between pools whose
+ * intra-tile layouts differ (LLMIG_LAYOUT_*) it moves each 16-bit element,
+ * again unchanged, to its place in the destination's layout.
  *
  * Error convention: every entry point returns LLMIG_OK (0) or a negative
  * code.  All argument checks run before anything is enqueued, so a call that
@@ -53,11 +55,32 @@ extern "C" {
 #define LLMIG_ERANGE (-3) /* a block id outside [0, num_blocks) */
 #define LLMIG_EHIP (-4)   /* the HIP runtime reported an error: see llmig_last_hip_error */
 
+/* Intra-tile layouts.  A (layer, K or V, block) tile holds block_size
+ * tokens x num_kv_heads heads x head_dim dims; x = 16 / elem_bytes dims make
+ * one 16-byte group.  Element (t, h, d) sits at element index
+ *   LLMIG_LAYOUT_NHD   (t * H + h) * D + d                 [block_size][H][D]
+ *                      (token-major: the pool layout above, FlashAttention-
+ *                      style engines)
+ *   LLMIG_LAYOUT_HND   (h * block_size + t) * D + d        [H][block_size][D]
+ *   LLMIG_LAYOUT_HCNX  ((h * D/x + d/x) * block_size + t) * x + d % x
+ *                                                          [H][D/x][block_size][x]
+ *                      (the key cache of vLLM's paged attention kernel)
+ *   LLMIG_LAYOUT_HDN   (h * D + d) * block_size + t        [H][D][block_size]
+ *                      (the value cache of vLLM's paged attention kernel)
+ * Migration between instances of one engine (§4.2) never converts; a pair
+ * of pools whose layouts differ converts inside the stage copy. */
+#define LLMIG_LAYOUT_NHD 0
+#define LLMIG_LAYOUT_HND 1
+#define LLMIG_LAYOUT_HCNX 2
+#define LLMIG_LAYOUT_HDN 3
+
 /* Describes a caller-owned pool.  k_ptrs and v_ptrs are HOST arrays of
- * num_layers DEVICE addresses, one per layer tensor
- * [num_blocks, block_size, num_kv_heads, head_dim]; each address must be
- * 16-byte aligned and tile_bytes a multiple of 16.  The arrays are read
- * during llmig_pool_create only. */
+ * num_layers DEVICE addresses, one per layer tensor of num_blocks tiles;
+ * each address must be 16-byte aligned and tile_bytes a multiple of 16.  The
+ * arrays are read during llmig_pool_create only.  k_layout and v_layout
+ * (LLMIG_LAYOUT_*, 0 = NHD) give the order of the elements inside the K and
+ * V tiles; HCNX needs elem_bytes to divide 16 and head_dim * elem_bytes to
+ * be a multiple of 16. */
 typedef struct llmig_pool_desc {
     int32_t num_layers;
     int32_t num_blocks;
@@ -67,6 +90,8 @@ typedef struct llmig_pool_desc {
     int32_t elem_bytes;
     const uint64_t *k_ptrs;
     const uint64_t *v_ptrs;
+    int32_t k_layout;
+    int32_t v_layout;
 } llmig_pool_desc;
 
 typedef struct llmig_pool llmig_pool;
@@ -133,7 +158,13 @@ int llmig_plan(const int32_t *src_table, int64_t src_table_len,
  * src and dst must be different pools whose layer, block_size, head and
  * element sizes match (num_blocks may differ) and whose memory does not
  * overlap; else LLMIG_EINVAL.  n = 0 does nothing.  A batched migration of
- * several requests concatenates their pairs into one call. */
+ * several requests concatenates their pairs into one call.
+ *
+ * When the pools' K or V layouts differ, every element of each tile moves
+ * to its place in the destination's layout (see LLMIG_LAYOUT_*).  That
+ * needs elem_bytes == 2, head_dim % 8 == 0, block_size % 8 == 0 if either
+ * side uses HDN, and block_size * head_dim * 2 <= 8192 (one head's slab of
+ * a tile); else LLMIG_EINVAL. */
 int llmig_stage(const llmig_pool *src, const llmig_pool *dst,
                 const int32_t *map_src, const int32_t *map_dst, int64_t n,
                 int map_on_device, void *stream);
@@ -141,6 +172,8 @@ int llmig_stage(const llmig_pool *src, const llmig_pool *dst,
 /* Block fusion, sending side (§5 "Block fusion"): gathers tiles of the
  * listed source blocks into the contiguous buffer `staging`, laid out
  * [num_layers][K=0, V=1][n][tile_bytes] with i in the order of blocks[].
+ * Tiles keep the pool's own intra-tile layout (pack and unpack never
+ * convert).
  * staging is device memory or pinned host memory mapped for the device
  * (hipHostMalloc); it is caller-owned, 16-byte aligned, and staging_bytes
  * must be at least n * num_layers * 2 * tile_bytes (else LLMIG_EINVAL).
@@ -159,7 +192,9 @@ int llmig_unpack(const llmig_pool *dst, const int32_t *blocks, int64_t n, int ma
  * token's K and V and leaves earlier ones unchanged): writes tokens
  * [from_tok, from_tok + n_tok) of a request into `pool` through its host
  * block table.  data is device memory laid out
- * [num_layers][K=0, V=1][n_tok][num_kv_heads * head_dim * elem_bytes].
+ * [num_layers][K=0, V=1][n_tok][num_kv_heads][head_dim] (elem_bytes each),
+ * and each element lands where the pool's layout puts it; a pool with a
+ * layout other than NHD needs elem_bytes == 2 and head_dim % 8 == 0.
  * table_len must cover the last token (LLMIG_EINVAL), ids are
  * range-checked (LLMIG_ERANGE).  Used to drive multi-stage migrations
  * without a model. */
@@ -276,8 +311,8 @@ int llmig_stream_read(const void *region, int64_t bytes, int32_t passes, int32_t
  * [num_layers][batch][q_heads][head_dim]; a sequence of length 0 gives
  * zeros.  workspace: device memory of at least the size
  * llmig_decode_attention_workspace returns for the same lengths.
- * Supported: head_dim 64 or 128, q_heads / num_kv_heads in {1, 2, 4, 8},
- * batch <= 256; else LLMIG_EINVAL.  Arithmetic in fp32. */
+ * Supported: NHD pools, head_dim 64 or 128, q_heads / num_kv_heads in
+ * {1, 2, 4, 8, 16}, batch <= 256; else LLMIG_EINVAL.  Arithmetic in fp32. */
 int llmig_decode_attention_workspace(const int32_t *ctx_lens, int32_t batch, int32_t num_layers,
                                      int32_t q_heads, int32_t head_dim, int64_t *bytes);
 int llmig_decode_attention(const llmig_pool *pool, int32_t dtype, const void *q, int32_t batch,

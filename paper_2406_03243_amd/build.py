@@ -10,7 +10,7 @@ import sys
 
 HERE = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(HERE)
-SOURCES = [os.path.join(HERE, "csrc", "llmig.hip")]   # includes csrc/common.h and csrc/copy_tiles.h
+SOURCES = [os.path.join(HERE, "csrc", "llmig.hip")]   # includes the other csrc/*.h
 LIBRARY = os.path.join(HERE, "libllmig.so")
 
 HIPCC_FLAGS = [

@@ -1,0 +1,266 @@
+// Cross-layout tile conversion: the stage copy between two pools that keep
+// the (token, head, dim) elements of a tile in different orders.  Part of
+// the single translation unit built from llmig.hip.
+//
+// What it computes: for every pair i, layer l and K/V, every element
+// (t, h, d) of tile (l, kv) of source block src[i] lands in tile (l, kv) of
+// destination block dst[i] at the position the destination's layout gives
+// it (the layouts are listed with LLMIG_LAYOUT_* in llmig.h).  Whole tiles
+// move, as in the same-layout copy (Llumnix §4.2), so a partial last block
+// carries its unused slots along.
+//
+// Kernel design (CDNA4, wave64):
+//  * In every layout a head's elements form one slab of block_size *
+//    head_dim * 2 bytes: contiguous in HND, HCNX and HDN, and block_size
+//    rows of head_dim * 2 bytes, one per token, in NHD.  A wavefront's work
+//    item is one (pair, layer, K/V, head) slab; it reads the slab with
+//    16-byte loads in the source's own order (whole rows, coalesced) and
+//    writes it with 16-byte stores in the destination's own order
+//    (contiguous), so neither side of HBM sees a partial row.
+//  * Between the two the slab passes through the wavefront's own LDS
+//    region, which is where the layouts transpose.  A 16-byte chunk is 8
+//    consecutive dims of one token in NHD, HND and HCNX, and 8 consecutive
+//    tokens of one dim in HDN.  Between the first three a chunk moves whole
+//    (one ds_read_b128 per chunk); to or from HDN every output chunk
+//    gathers 8 16-bit elements from 8 source chunks.  The LDS image has one
+//    16-byte pad after every 16 chunks, which spreads the strided reads of
+//    both cases over distinct banks for the common shapes (block_size 16,
+//    head_dim 64 or 128).
+//  * A plane whose two layouts agree (say K converts and V does not) moves
+//    chunk for chunk, registers straight to the store, without LDS.
+//  * Index arithmetic divides chunk numbers (< 2^16) by per-call constants
+//    with a multiply-high by ceil(2^32 / divisor), exact in that range.
+//  * Block ids, layouts and base addresses are wavefront-uniform and come
+//    from the kernel arguments or scalar loads; ids of up to kInlinePairs
+//    pairs travel inline, as in the same-layout copy.
+#pragma once
+
+#include <algorithm>
+#include <cstring>
+
+#include "common.h"
+
+namespace {
+
+constexpr int kMaxSlabChunksPerLane = 8;            // slabs of up to 8 KiB
+
+struct ConvertArgs {
+    const uint64_t *src_tab;
+    const uint64_t *dst_tab;
+    const int32_t *src_ids_dev; // device id lists (null when the ids are inline)
+    const int32_t *dst_ids_dev;
+    uint64_t magic_row;         // ceil(2^32 / row_chunks)
+    uint64_t magic_bs;          // ceil(2^32 / block_size)
+    uint64_t magic_t;           // ceil(2^32 / t_chunks)
+    uint32_t tile_bytes;
+    uint32_t num_layers;
+    uint32_t heads;
+    uint32_t block_size;
+    uint32_t row_chunks;        // head_dim / 8: chunks of one token's head
+    uint32_t t_chunks;          // block_size / 8: chunks of one dim's tokens (HDN)
+    uint32_t chunks;            // chunks of one head slab
+    uint32_t units;             // wave items: pairs * 2 * num_layers * heads
+    int32_t layouts[4];         // source K, source V, destination K, destination V
+    int32_t src_ids[kInlinePairs];
+    int32_t dst_ids[kInlinePairs];
+};
+
+__device__ __forceinline__ uint32_t div_magic(uint32_t n, uint64_t magic)
+{
+    return static_cast<uint32_t>((static_cast<uint64_t>(n) * magic) >> 32);
+}
+
+// Byte offset inside a tile of chunk k (in the layout's own order) of head h.
+__device__ __forceinline__ uint32_t slab_offset(int32_t layout, uint32_t h, uint32_t k, const ConvertArgs &a)
+{
+    if (layout == LLMIG_LAYOUT_NHD) {
+        const uint32_t t = div_magic(k, a.magic_row);
+        const uint32_t c = k - t * a.row_chunks;
+        return ((t * a.heads + h) * a.row_chunks + c) * 16u;
+    }
+    return (h * a.chunks + k) * 16u;
+}
+
+// Slab index of the chunk holding dims [8c, 8c + 8) of token t, in a layout
+// whose chunks run along the dims (NHD, HND, HCNX).
+__device__ __forceinline__ uint32_t dim_chunk_index(int32_t layout, uint32_t t, uint32_t c, const ConvertArgs &a)
+{
+    return layout == LLMIG_LAYOUT_HCNX ? c * a.block_size + t : t * a.row_chunks + c;
+}
+
+__device__ __forceinline__ uint32_t padded(uint32_t k)
+{
+    return k + (k >> 4);
+}
+
+__device__ __forceinline__ void wave_lds_sync()
+{
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+}
+
+template <bool INLINE_IDS, int N>
+__global__ void __launch_bounds__(kThreads) convert_tiles(const ConvertArgs a)
+{
+    __shared__ u32x4 lds[kThreads / 64][68 * N];     // 64 N chunks + one pad per 16
+    const uint32_t lane = threadIdx.x % 64;
+    const uint32_t wave = threadIdx.x / 64;
+    u32x4 *mine = lds[wave];
+    const uint16_t *mine16 = reinterpret_cast<const uint16_t *>(mine);
+    const uint32_t waves = gridDim.x * (kThreads / 64);
+    const uint32_t per_pair_plane = a.heads;
+    const uint32_t planes = 2u * a.num_layers;
+
+    for (uint32_t w = blockIdx.x * (kThreads / 64) + wave; w < a.units; w += waves) {
+        const uint32_t unit = uniform(w);
+        const uint32_t tile = unit / per_pair_plane;
+        const uint32_t h = unit - tile * per_pair_plane;
+        const uint32_t i = tile / planes;
+        const uint32_t plane = tile - i * planes;
+        const uint32_t layer = plane >> 1, kv = plane & 1u;
+        const int32_t sl = a.layouts[kv], dl = a.layouts[2 + kv];
+
+        const int32_t sid = INLINE_IDS ? a.src_ids[i] : id_entry(a.src_ids_dev, i);
+        const int32_t did = INLINE_IDS ? a.dst_ids[i] : id_entry(a.dst_ids_dev, i);
+        const uint8_t *s = reinterpret_cast<const uint8_t *>(table_entry(a.src_tab, kv * a.num_layers + layer)) +
+                           static_cast<uint64_t>(uniform(static_cast<uint32_t>(sid))) * a.tile_bytes;
+        uint8_t *d = reinterpret_cast<uint8_t *>(table_entry(a.dst_tab, kv * a.num_layers + layer)) +
+                     static_cast<uint64_t>(uniform(static_cast<uint32_t>(did))) * a.tile_bytes;
+
+        u32x4 r[N];
+#pragma unroll
+        for (int u = 0; u < N; ++u) {
+            const uint32_t k = lane + 64u * u;
+            if (k < a.chunks)
+                r[u] = load16(s + slab_offset(sl, h, k, a));
+        }
+        if (sl == dl) {
+#pragma unroll
+            for (int u = 0; u < N; ++u) {
+                const uint32_t k = lane + 64u * u;
+                if (k < a.chunks)
+                    store16(d + slab_offset(dl, h, k, a), r[u]);
+            }
+            continue;
+        }
+#pragma unroll
+        for (int u = 0; u < N; ++u) {
+            const uint32_t k = lane + 64u * u;
+            if (k < a.chunks)
+                mine[padded(k)] = r[u];
+        }
+        wave_lds_sync();
+#pragma unroll
+        for (int u = 0; u < N; ++u) {
+            const uint32_t k = lane + 64u * u;
+            if (k >= a.chunks)
+                continue;
+            u32x4 v;
+            if (dl == LLMIG_LAYOUT_HDN) {
+                // Output chunk: tokens [8 tg, 8 tg + 8) of dim dd.
+                const uint32_t dd = div_magic(k, a.magic_t);
+                const uint32_t tg = k - dd * a.t_chunks;
+                const uint32_t c = dd >> 3, e = dd & 7u;
+                uint32_t x[8];
+#pragma unroll
+                for (int j = 0; j < 8; ++j)
+                    x[j] = mine16[padded(dim_chunk_index(sl, 8u * tg + j, c, a)) * 8u + e];
+                v = u32x4{x[0] | (x[1] << 16), x[2] | (x[3] << 16), x[4] | (x[5] << 16), x[6] | (x[7] << 16)};
+            } else {
+                // Output chunk: dims [8 c, 8 c + 8) of token t.
+                uint32_t t, c;
+                if (dl == LLMIG_LAYOUT_HCNX) {
+                    c = div_magic(k, a.magic_bs);
+                    t = k - c * a.block_size;
+                } else {
+                    t = div_magic(k, a.magic_row);
+                    c = k - t * a.row_chunks;
+                }
+                if (sl == LLMIG_LAYOUT_HDN) {
+                    const uint32_t tg = t >> 3, e = t & 7u;
+                    uint32_t x[8];
+#pragma unroll
+                    for (int j = 0; j < 8; ++j)
+                        x[j] = mine16[padded((8u * c + j) * a.t_chunks + tg) * 8u + e];
+                    v = u32x4{x[0] | (x[1] << 16), x[2] | (x[3] << 16), x[4] | (x[5] << 16),
+                              x[6] | (x[7] << 16)};
+                } else {
+                    v = mine[padded(dim_chunk_index(sl, t, c, a))];
+                }
+            }
+            store16(d + slab_offset(dl, h, k, a), v);
+        }
+        wave_lds_sync();
+    }
+}
+
+template <bool INLINE_IDS>
+const void *convert_kernel_n(int n)
+{
+    switch (n) {
+    case 8:
+        return reinterpret_cast<const void *>(&convert_tiles<INLINE_IDS, 8>);
+    case 4:
+        return reinterpret_cast<const void *>(&convert_tiles<INLINE_IDS, 4>);
+    case 2:
+        return reinterpret_cast<const void *>(&convert_tiles<INLINE_IDS, 2>);
+    default:
+        return reinterpret_cast<const void *>(&convert_tiles<INLINE_IDS, 1>);
+    }
+}
+
+uint64_t magic_for(uint32_t divisor)
+{
+    return ((1ull << 32) + divisor - 1) / divisor;
+}
+
+// Chunks per lane (a power of two) for slabs of `chunks` 16-byte chunks.
+int convert_chunks_per_lane(uint32_t chunks)
+{
+    int n = 1;
+    while (static_cast<uint32_t>(n) * 64u < chunks)
+        n *= 2;
+    return n;
+}
+
+// Launches the conversion of n pairs.  The caller has checked that the
+// geometry is supported (16-bit elements, head_dim % 8 == 0, block_size % 8
+// == 0 when a side is HDN, slabs of at most 8 KiB).
+int launch_convert(ConvertArgs a, const int32_t *src_ids, const int32_t *dst_ids, int64_t n, bool ids_on_device,
+                   hipStream_t stream, uint32_t max_workgroups)
+{
+    const int per_lane = convert_chunks_per_lane(a.chunks);
+    if (per_lane > kMaxSlabChunksPerLane)
+        return LLMIG_EINVAL;
+    a.magic_row = magic_for(a.row_chunks);
+    a.magic_bs = magic_for(a.block_size);
+    a.magic_t = magic_for(a.t_chunks > 0 ? a.t_chunks : 1u);
+    const uint64_t units_per_pair = 2ull * a.num_layers * a.heads;
+    const uint64_t per_launch = std::min<uint64_t>(0x7fffffffull / units_per_pair,
+                                                   ids_on_device ? UINT64_MAX : kInlinePairs);
+    if (per_launch == 0)
+        return LLMIG_EINVAL;
+    const void *fn = ids_on_device ? convert_kernel_n<false>(per_lane) : convert_kernel_n<true>(per_lane);
+    for (int64_t first = 0; first < n; first += static_cast<int64_t>(per_launch)) {
+        const uint32_t m = static_cast<uint32_t>(std::min<int64_t>(n - first, per_launch));
+        a.units = static_cast<uint32_t>(m * units_per_pair);
+        if (ids_on_device) {
+            a.src_ids_dev = src_ids + first;
+            a.dst_ids_dev = dst_ids + first;
+        } else {
+            std::memcpy(a.src_ids, src_ids + first, m * sizeof(int32_t));
+            std::memcpy(a.dst_ids, dst_ids + first, m * sizeof(int32_t));
+        }
+        void *args[] = {&a};
+        uint32_t grid = (a.units + kThreads / 64 - 1) / (kThreads / 64);
+        if (max_workgroups > 0)
+            grid = std::min(grid, max_workgroups);
+        hipError_t e = hipLaunchKernel(fn, dim3(grid), dim3(kThreads), args, 0, stream);
+        if (e != hipSuccess)
+            return hip_error(e);
+    }
+    return LLMIG_OK;
+}
+
+} // namespace

@@ -188,7 +188,8 @@ int launch_copy(CopyArgs a, const int32_t *src_ids, const int32_t *dst_ids, int6
     }
     a.spans_per_tile = spt;
     const uint64_t items_per_pair = 2ull * a.num_layers * spt;
-    uint64_t per_launch = ids_on_device ? (0x7fffffffull / items_per_pair) : kInlinePairs;
+    uint64_t per_launch = std::min<uint64_t>(0x7fffffffull / items_per_pair,
+                                             ids_on_device ? UINT64_MAX : kInlinePairs);
     if (per_launch == 0)
         return LLMIG_EINVAL;
     a.lin_pairs = static_cast<uint32_t>(n);

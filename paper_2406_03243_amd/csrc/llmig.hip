@@ -21,11 +21,13 @@
 
 #include "llmig.h"
 #include "common.h"
+#include "convert_tiles.h"
 #include "copy_tiles.h"
 #include "decode_attention.h"
 
 struct llmig_pool {
     int32_t num_layers, num_blocks, block_size, num_kv_heads, head_dim, elem_bytes;
+    int32_t layouts[2];                               // K, V intra-tile layouts (LLMIG_LAYOUT_*)
     int64_t tile_bytes;
     int device;
     uint64_t *d_tab;                                  // device [2 * L]: K bases, then V bases
@@ -53,6 +55,9 @@ struct WriteArgs {
     uint32_t tile_bytes;
     uint32_t block_size;
     uint32_t num_layers;
+    uint32_t head_dim;
+    uint32_t row_chunks;   // head_dim * elem_bytes / 16 (layouts other than NHD)
+    int32_t layouts[2];    // K, V
     uint32_t data_tokens;  // tokens in the whole call (plane stride of data)
     uint32_t first_token;  // this launch's first token within the call
     uint32_t tokens;       // tokens in this launch
@@ -70,13 +75,36 @@ __global__ void __launch_bounds__(kThreads) write_token_slots(const WriteArgs a)
         const uint32_t rel = a.first_slot + j;
         const uint32_t blk = rel / a.block_size;
         const uint32_t slot = rel - blk * a.block_size;
-        uint8_t *d = reinterpret_cast<uint8_t *>(table_entry(a.tab, kv * a.num_layers + layer)) +
-                     static_cast<uint64_t>(uniform(static_cast<uint32_t>(a.ids[blk]))) * a.tile_bytes +
-                     static_cast<uint64_t>(slot) * a.slot_bytes;
+        uint8_t *tile = reinterpret_cast<uint8_t *>(table_entry(a.tab, kv * a.num_layers + layer)) +
+                        static_cast<uint64_t>(uniform(static_cast<uint32_t>(a.ids[blk]))) * a.tile_bytes;
         const uint8_t *s = a.data + (static_cast<uint64_t>(plane) * a.data_tokens + a.first_token + j) *
                                         a.slot_bytes;
-        for (uint32_t off = threadIdx.x * 16u; off < a.slot_bytes; off += kRowBytes)
-            *(LLMIG_GLOBAL u32x4 *)(d + off) = load16(s + off);
+        const int32_t layout = a.layouts[kv];
+        if (layout == LLMIG_LAYOUT_NHD) {
+            uint8_t *d = tile + static_cast<uint64_t>(slot) * a.slot_bytes;
+            for (uint32_t off = threadIdx.x * 16u; off < a.slot_bytes; off += kRowBytes)
+                *(LLMIG_GLOBAL u32x4 *)(d + off) = load16(s + off);
+            continue;
+        }
+        // 16-bit elements: chunk q of the token is dims [8c, 8c + 8) of head h.
+        for (uint32_t off = threadIdx.x * 16u; off < a.slot_bytes; off += kRowBytes) {
+            const uint32_t q = off / 16u;
+            const uint32_t h = q / a.row_chunks, c = q - h * a.row_chunks;
+            const u32x4 v = load16(s + off);
+            if (layout == LLMIG_LAYOUT_HND) {
+                *(LLMIG_GLOBAL u32x4 *)(tile + ((h * a.block_size + slot) * a.row_chunks + c) * 16u) = v;
+            } else if (layout == LLMIG_LAYOUT_HCNX) {
+                *(LLMIG_GLOBAL u32x4 *)(tile + ((h * a.row_chunks + c) * a.block_size + slot) * 16u) = v;
+            } else {
+                const uint32_t w[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+                for (uint32_t e = 0; e < 8; ++e) {
+                    const uint32_t dim = 8u * c + e;
+                    *(LLMIG_GLOBAL uint16_t *)(tile + ((h * a.head_dim + dim) * a.block_size + slot) * 2u) =
+                        static_cast<uint16_t>(w[e / 2] >> (16u * (e & 1u)));
+                }
+            }
+        }
     }
 }
 
@@ -216,9 +244,29 @@ int fused_copy_checks(const llmig_pool *pool, const int32_t *blocks, int64_t n, 
     return LLMIG_OK;
 }
 
+bool same_layouts(const llmig_pool *src, const llmig_pool *dst)
+{
+    return src->layouts[0] == dst->layouts[0] && src->layouts[1] == dst->layouts[1];
+}
+
+// Whether a stage between pools of these (equal) geometries and these
+// layouts is supported by the conversion kernel.
+bool conversion_supported(const llmig_pool *src, const llmig_pool *dst)
+{
+    if (src->elem_bytes != 2 || src->head_dim % 8 != 0)
+        return false;
+    const bool hdn = src->layouts[0] == LLMIG_LAYOUT_HDN || src->layouts[1] == LLMIG_LAYOUT_HDN ||
+                     dst->layouts[0] == LLMIG_LAYOUT_HDN || dst->layouts[1] == LLMIG_LAYOUT_HDN;
+    if (hdn && src->block_size % 8 != 0)
+        return false;
+    const int64_t chunks = static_cast<int64_t>(src->block_size) * src->head_dim / 8;
+    return chunks <= 64 * kMaxSlabChunksPerLane;
+}
+
 bool pools_compatible(const llmig_pool *src, const llmig_pool *dst)
 {
-    return same_geometry(src, dst) && src->device == dst->device && !pools_overlap(src, dst);
+    return same_geometry(src, dst) && src->device == dst->device && !pools_overlap(src, dst) &&
+           (same_layouts(src, dst) || conversion_supported(src, dst));
 }
 
 int check_pair_ids(const llmig_pool *src, const llmig_pool *dst, const int32_t *ms, const int32_t *md, int64_t n)
@@ -230,6 +278,24 @@ int check_pair_ids(const llmig_pool *src, const llmig_pool *dst, const int32_t *
 int launch_stage(const llmig_pool *src, const llmig_pool *dst, const int32_t *ms, const int32_t *md, int64_t n,
                  bool ids_on_device, hipStream_t stream, uint32_t max_workgroups = 0)
 {
+    if (!same_layouts(src, dst)) {
+        ConvertArgs c;
+        std::memset(&c, 0, sizeof(c));
+        c.src_tab = src->d_tab;
+        c.dst_tab = dst->d_tab;
+        c.tile_bytes = static_cast<uint32_t>(src->tile_bytes);
+        c.num_layers = static_cast<uint32_t>(src->num_layers);
+        c.heads = static_cast<uint32_t>(src->num_kv_heads);
+        c.block_size = static_cast<uint32_t>(src->block_size);
+        c.row_chunks = static_cast<uint32_t>(src->head_dim / 8);
+        c.t_chunks = static_cast<uint32_t>(src->block_size / 8);
+        c.chunks = static_cast<uint32_t>(src->block_size * src->head_dim / 8);
+        c.layouts[0] = src->layouts[0];
+        c.layouts[1] = src->layouts[1];
+        c.layouts[2] = dst->layouts[0];
+        c.layouts[3] = dst->layouts[1];
+        return launch_convert(c, ms, md, n, ids_on_device, stream, max_workgroups);
+    }
     CopyArgs a;
     std::memset(&a, 0, sizeof(a));
     a.src_tab = src->d_tab;
@@ -275,6 +341,13 @@ int llmig_pool_create(const llmig_pool_desc *desc, llmig_pool **out)
                          desc->elem_bytes;
     if (tile % 16 != 0 || tile > 0x7fffffffLL)
         return LLMIG_EINVAL;
+    for (int32_t layout : {desc->k_layout, desc->v_layout}) {
+        if (layout < LLMIG_LAYOUT_NHD || layout > LLMIG_LAYOUT_HDN)
+            return LLMIG_EINVAL;
+        if (layout == LLMIG_LAYOUT_HCNX &&
+            (16 % desc->elem_bytes != 0 || (static_cast<int64_t>(desc->head_dim) * desc->elem_bytes) % 16 != 0))
+            return LLMIG_EINVAL;
+    }
     const int32_t L = desc->num_layers;
     std::vector<uint64_t> tab(2 * static_cast<size_t>(L));
     for (int32_t l = 0; l < L; ++l) {
@@ -294,6 +367,8 @@ int llmig_pool_create(const llmig_pool_desc *desc, llmig_pool **out)
     pool->num_kv_heads = desc->num_kv_heads;
     pool->head_dim = desc->head_dim;
     pool->elem_bytes = desc->elem_bytes;
+    pool->layouts[0] = desc->k_layout;
+    pool->layouts[1] = desc->v_layout;
     pool->tile_bytes = tile;
     const uint64_t tensor_bytes = static_cast<uint64_t>(tile) * static_cast<uint64_t>(desc->num_blocks);
     for (uint64_t p : tab)
@@ -588,6 +663,9 @@ int llmig_write_tokens(const llmig_pool *pool, const int32_t *table, int64_t tab
     if (!table || !data || (reinterpret_cast<uintptr_t>(data) & 15u) || slot_bytes % 16 != 0 ||
         n_tok > 0x7fffffffLL / (2 * pool->num_layers))
         return LLMIG_EINVAL;
+    const bool nhd = pool->layouts[0] == LLMIG_LAYOUT_NHD && pool->layouts[1] == LLMIG_LAYOUT_NHD;
+    if (!nhd && (pool->elem_bytes != 2 || pool->head_dim % 8 != 0))
+        return LLMIG_EINVAL;
     const int64_t bs = pool->block_size;
     const int64_t first_blk = from_tok / bs, last_blk = (from_tok + n_tok - 1) / bs;
     if (last_blk >= table_len)
@@ -603,6 +681,10 @@ int llmig_write_tokens(const llmig_pool *pool, const int32_t *table, int64_t tab
     a.tile_bytes = static_cast<uint32_t>(pool->tile_bytes);
     a.block_size = static_cast<uint32_t>(bs);
     a.num_layers = static_cast<uint32_t>(pool->num_layers);
+    a.head_dim = static_cast<uint32_t>(pool->head_dim);
+    a.row_chunks = static_cast<uint32_t>(pool->head_dim / 8);
+    a.layouts[0] = pool->layouts[0];
+    a.layouts[1] = pool->layouts[1];
     a.data_tokens = static_cast<uint32_t>(n_tok);
     // Each launch covers whole blocks' worth of tokens, at most kInlinePairs blocks.
     int64_t t = from_tok;
@@ -678,7 +760,8 @@ int llmig_decode_attention(const llmig_pool *pool, int32_t dtype, const void *q,
                            void *workspace, int64_t workspace_bytes, float *out, void *stream)
 {
     if (!pool || (dtype != 0 && dtype != 1) || pool->elem_bytes != 2 || !q || !tables || !ctx_lens || !out ||
-        batch < 1 || batch > kAttnMaxBatch || q_heads < 1 || table_stride < 1)
+        batch < 1 || batch > kAttnMaxBatch || q_heads < 1 || table_stride < 1 ||
+        pool->layouts[0] != LLMIG_LAYOUT_NHD || pool->layouts[1] != LLMIG_LAYOUT_NHD)
         return LLMIG_EINVAL;
     const int32_t D = pool->head_dim, hkv = pool->num_kv_heads;
     if (q_heads % hkv != 0)

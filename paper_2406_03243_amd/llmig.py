@@ -40,7 +40,14 @@ class _PoolDesc(ctypes.Structure):
     _fields_ = [("num_layers", ctypes.c_int32), ("num_blocks", ctypes.c_int32),
                 ("block_size", ctypes.c_int32), ("num_kv_heads", ctypes.c_int32),
                 ("head_dim", ctypes.c_int32), ("elem_bytes", ctypes.c_int32),
-                ("k_ptrs", ctypes.POINTER(ctypes.c_uint64)), ("v_ptrs", ctypes.POINTER(ctypes.c_uint64))]
+                ("k_ptrs", ctypes.POINTER(ctypes.c_uint64)), ("v_ptrs", ctypes.POINTER(ctypes.c_uint64)),
+                ("k_layout", ctypes.c_int32), ("v_layout", ctypes.c_int32)]
+
+
+# Intra-tile layouts (LLMIG_LAYOUT_*): NHD [block_size][heads][head_dim],
+# HND [heads][block_size][head_dim], HCNX [heads][head_dim/x][block_size][x]
+# with x = 16 / elem_bytes, HDN [heads][head_dim][block_size].
+LAYOUT_NHD, LAYOUT_HND, LAYOUT_HCNX, LAYOUT_HDN = 0, 1, 2, 3
 
 
 _i32p = ctypes.POINTER(ctypes.c_int32)
@@ -126,9 +133,11 @@ def _ids(a):
 class Pool:
     """A registered KV block pool: per-layer K and V tensors of shape
     [num_blocks, block_size, num_kv_heads, head_dim] on one GPU.  The tensors
-    stay owned by the caller; the handle keeps references to them."""
+    stay owned by the caller; the handle keeps references to them.
+    ``layouts`` gives the (K, V) intra-tile layouts: the bytes of each
+    block follow them, whatever the tensors' own shape suggests."""
 
-    def __init__(self, k_layers, v_layers):
+    def __init__(self, k_layers, v_layers, layouts=(LAYOUT_NHD, LAYOUT_NHD)):
         if len(k_layers) != len(v_layers) or not k_layers:
             raise ValueError("need one K and one V tensor per layer")
         t0 = k_layers[0]
@@ -141,13 +150,14 @@ class Pool:
         vp = (ctypes.c_uint64 * len(v_layers))(*[t.data_ptr() for t in v_layers])
         desc = _PoolDesc(len(k_layers), nb, bs, heads, dim, t0.element_size(),
                          ctypes.cast(kp, ctypes.POINTER(ctypes.c_uint64)),
-                         ctypes.cast(vp, ctypes.POINTER(ctypes.c_uint64)))
+                         ctypes.cast(vp, ctypes.POINTER(ctypes.c_uint64)), int(layouts[0]), int(layouts[1]))
         handle = _vp()
         _check(_lib.llmig_pool_create(ctypes.byref(desc), ctypes.byref(handle)), "llmig_pool_create")
         self._handle = handle
         self.k, self.v = list(k_layers), list(v_layers)
         self.num_layers, self.num_blocks, self.block_size = len(k_layers), nb, bs
         self.num_kv_heads, self.head_dim, self.elem_bytes = heads, dim, t0.element_size()
+        self.layouts = (int(layouts[0]), int(layouts[1]))
         self.tile_bytes = _lib.llmig_pool_tile_bytes(handle)
         self.slot_bytes = self.tile_bytes // bs
 

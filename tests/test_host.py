@@ -141,9 +141,17 @@ def test_pool_desc_validation_without_gpu():
         (2, 4, 16, 1, 8, 2, bad_align, ptrs),
         (2, 4, 16, 1, 8, 2, ptrs, overlap),
     ]
-    for L, nb, bs, h, d, e, kp, vp in cases:
+    other = (ctypes.c_uint64 * 2)(0x100000, 0x200000)
+    layout_cases = [
+        (2, 4, 16, 1, 8, 2, ptrs, other, 4, 0),                       # no such layout
+        (2, 4, 16, 1, 8, 2, ptrs, other, 0, -1),
+        (2, 4, 16, 1, 4, 2, ptrs, other, llmig.LAYOUT_HCNX, 0),       # head_dim * 2 not a multiple of 16
+        (2, 4, 16, 3, 16, 1, ptrs, ptrs, llmig.LAYOUT_HDN, 0),        # a valid layout; K and V share memory
+    ]
+    for L, nb, bs, h, d, e, kp, vp, *lay in cases + layout_cases:
+        lk, lv = lay if lay else (0, 0)
         desc = llmig._PoolDesc(L, nb, bs, h, d, e, ctypes.cast(kp, ctypes.POINTER(ctypes.c_uint64)),
-                               ctypes.cast(vp, ctypes.POINTER(ctypes.c_uint64)))
+                               ctypes.cast(vp, ctypes.POINTER(ctypes.c_uint64)), lk, lv)
         assert lib.llmig_pool_create(ctypes.byref(desc), ctypes.byref(out)) == llmig.LLMIG_EINVAL
         assert not out.value
 
