@@ -86,8 +86,9 @@ def main():
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--cpu-seconds", type=float, default=10.0, help="CPU oracle sample budget")
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--sections", default="downtime,batched,load",
-                    help="extra workloads after the main one (comma list of downtime, batched, load; empty for none)")
+    ap.add_argument("--sections", default="downtime,batched,load,xlayout",
+                    help="extra workloads after the main one (comma list of downtime, batched, load, xlayout;"
+                         " empty for none)")
     ap.add_argument("--downtime-reps", type=int, default=7)
     ap.add_argument("--no-gc-freeze", action="store_true", help="leave set-up objects to the collector")
     ap.add_argument("--calibration-copy", action="store_true",
@@ -240,6 +241,9 @@ def main():
     if "load" in sections:
         result["under_load"] = load_section()
         torch.cuda.empty_cache()
+    if "xlayout" in sections:
+        result["cross_layout"] = xlayout_section()
+        torch.cuda.empty_cache()
 
     print(json.dumps(result), flush=True)
 
@@ -376,6 +380,60 @@ def batched_section(reps=10, host_reps=3, chunk_pairs=64):
         ht = statistics.median(host_times)
         out["host_staged"][mode] = {"seconds_median": round(ht, 4), "GBps_each_way": round(one_way / ht / 1e9, 2)}
     su.close()
+    return out
+
+
+def xlayout_section(reps=10):
+    """Stage 1 of the LLaMA-7B migration (512 blocks, 4 GiB each way) between
+    pools of different intra-tile layouts: the same tensors registered under
+    several layouts, timed per layout pair with events on the stage's stream."""
+    import torch
+
+    from paper_2406_03243_amd import harness, scenarios
+    from paper_2406_03243_amd import workloads as wl
+    from paper_2406_03243_amd.llmig import (LAYOUT_HCNX, LAYOUT_HDN, LAYOUT_HND, LAYOUT_NHD, Pool,
+                                            llmig_stage)
+
+    w = wl.LLAMA7B
+    shape = w.shape
+    sk, sv = harness.alloc_layers(shape)
+    dk, dv = harness.alloc_layers(shape)
+    harness.fill_on_device(sk + sv, w.seed * 16 + wl.SRC_VALUES)
+    harness.fill_on_device(dk + dv, w.seed * 16 + wl.DST_VALUES)
+    table, _ = wl.request_table(w.seed, shape.num_blocks, w.table_blocks, w.src_preoccupied)
+    free, _ = wl.free_list(w.seed, shape.num_blocks, w.dst_preoccupied)
+    n = w.lengths[0] // shape.block_size
+    ms, md = table[:n], free[:n]
+    names = {LAYOUT_NHD: "NHD", LAYOUT_HND: "HND", LAYOUT_HCNX: "HCNX", LAYOUT_HDN: "HDN"}
+    cases = [((LAYOUT_NHD, LAYOUT_NHD), (LAYOUT_NHD, LAYOUT_NHD)),      # same layout: the tile copy
+             ((LAYOUT_NHD, LAYOUT_NHD), (LAYOUT_HND, LAYOUT_HND)),      # chunks move whole
+             ((LAYOUT_NHD, LAYOUT_NHD), (LAYOUT_HCNX, LAYOUT_HDN)),     # token-major -> vLLM paged attention
+             ((LAYOUT_HCNX, LAYOUT_HDN), (LAYOUT_NHD, LAYOUT_NHD))]     # and back
+    nbytes = stage_bytes(n, shape, 2 * shape.block_size * shape.kv_heads * shape.head_dim)
+    out = {"workload": w.name, "pairs": int(n), "bytes": nbytes, "cases": []}
+    mig = torch.cuda.Stream()
+    for sl, dl in cases:
+        src, dst = Pool(sk, sv, layouts=sl), Pool(dk, dv, layouts=dl)
+        for _ in range(3):
+            llmig_stage(src, dst, ms, md, stream=mig)
+        torch.cuda.synchronize()
+        times = []
+        for _ in range(reps):
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record(mig)
+            llmig_stage(src, dst, ms, md, stream=mig)
+            e1.record(mig)
+            torch.cuda.synchronize()
+            times.append(e0.elapsed_time(e1) * 1e3)
+        us = statistics.median(times)
+        gbs = nbytes / (us * 1e-6) / 1e9
+        out["cases"].append({"src": "/".join(names[x] for x in sl), "dst": "/".join(names[x] for x in dl),
+                             "stage_us_median": round(us, 1), "GBps": round(gbs, 1),
+                             "hbm_frac": round(gbs / HBM_PEAK_GBS, 3)})
+        log("cross-layout", out["cases"][-1])
+        src.close()
+        dst.close()
+    del sk, sv, dk, dv
     return out
 
 

@@ -219,3 +219,43 @@ def test_gqa_long_under_load():
     # the reader really read: its sums are not all zero
     assert bool((sink != 0).any())
     su.close()
+
+
+@pytest.mark.parametrize("layouts", [((0, 0), (1, 1)), ((0, 0), (2, 3)), ((2, 3), (0, 0))],
+                         ids=["NHD_to_HND", "NHD_to_HCNX_HDN", "HCNX_HDN_to_NHD"])
+def test_llama7b_cross_layout_stage(layouts):
+    """Stage 1 of the benchmark's LLaMA-7B migration (512 pairs, 4 GiB each
+    way) between pools of different intra-tile layouts, launched as the
+    benchmark's cross-layout section launches it.  A sample of 48 pairs is
+    replayed by the oracle; every pair is converted back into free blocks of
+    the source pool and compared with its source tile on the device."""
+    from paper_2406_03243_amd.llmig import Pool
+    sl, dl = layouts
+    w = wl.LLAMA7B
+    shape = w.shape
+    say("llama7b cross-layout stage", sl, dl)
+    sk, sv = harness.alloc_layers(shape)
+    dk, dv = harness.alloc_layers(shape)
+    harness.fill_on_device(sk + sv, w.seed * 16 + wl.SRC_VALUES)
+    harness.fill_on_device(dk + dv, w.seed * 16 + wl.DST_VALUES)
+    table, _ = wl.request_table(w.seed, shape.num_blocks, w.table_blocks, w.src_preoccupied)
+    free, _ = wl.free_list(w.seed, shape.num_blocks, w.dst_preoccupied)
+    n = w.lengths[0] // shape.block_size
+    ms, md = table[:n], free[:n]
+    src, dst = Pool(sk, sv, layouts=sl), Pool(dk, dv, layouts=dl)
+    pick = np.sort(wl.stream(w.seed, wl.EXTRA, 9).choice(n, 48, replace=False))
+    hs, hd = compact(src, ms[pick]), compact(dst, md[pick])
+    guard = untouched_sample(dst, md, 256, 2)
+    guard_before = compact(dst, guard)
+    llmig_stage(src, dst, ms, md)
+    torch.cuda.synchronize()
+    ids = np.arange(len(pick), dtype=np.int32)
+    oracle.default().copy_layout(hs, sl, hd, dl, ids, ids, shape.kv_heads, shape.head_dim, 2)
+    assert_same(compact(dst, md[pick]), hd, "destination sample")
+    assert_same(compact(dst, guard), guard_before, "blocks outside the mapping")
+    spare = wl.stream(w.seed, wl.EXTRA, 10).permutation(np.setdiff1d(np.arange(shape.num_blocks), ms))[:n]
+    llmig_stage(dst, src, md, spare.astype(np.int32))
+    torch.cuda.synchronize()
+    assert device_pairs_equal(src, src, ms, spare), "round trip differs from the source"
+    src.close()
+    dst.close()
