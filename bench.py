@@ -74,6 +74,23 @@ def bulk_span_rows(tile_bytes: int) -> int:
     return span
 
 
+def percentile(xs, q):
+    """The q-th percentile (0-100) of xs, linear between order statistics."""
+    v = sorted(xs)
+    if len(v) == 1:
+        return v[0]
+    pos = (len(v) - 1) * q / 100.0
+    lo = int(pos)
+    hi = min(lo + 1, len(v) - 1)
+    return v[lo] + (v[hi] - v[lo]) * (pos - lo)
+
+
+def spread(us):
+    """Median, p10 and p90 of a list of durations, rounded."""
+    return {"median": round(statistics.median(us), 2), "p10": round(percentile(us, 10), 2),
+            "p90": round(percentile(us, 90), 2), "n": len(us)}
+
+
 def stage_bytes(blocks, shape, tile_bytes):
     """Algorithmic bytes of a stage: every tile read once and written once."""
     return 2 * blocks * shape.num_layers * 2 * tile_bytes
@@ -177,6 +194,7 @@ def main():
         entry = {"tokens": [rec.from_tok, rec.to_tok], "blocks": rec.blocks, "bytes": b, "final": rec.final}
         if us:
             entry["gpu_us_median"] = round(statistics.median(us), 2)
+            entry["gpu_us"] = spread(us)
             entry["GBps"] = round(b / (statistics.median(us) * 1e-6) / 1e9, 1)
         stages.append(entry)
 
@@ -250,7 +268,9 @@ def main():
 
 def cpu_baseline(src, table, free, stage1, shape, seconds):
     """The oracle's per-tile copy on host snapshots of a sample of stage 1's
-    blocks, single-threaded, repeated for about ``seconds``."""
+    blocks: one thread for 0.4 x ``seconds``, then every core of the
+    process's CPU share (at most 16) on disjoint slices, about 2 x
+    ``seconds`` of CPU work in all.  ``value`` is the all-core rate."""
     import numpy as np
 
     import oracle
@@ -268,18 +288,48 @@ def cpu_baseline(src, table, free, stage1, shape, seconds):
     ids = np.arange(n, dtype=np.int32)
     orc = oracle.default()
     orc.copy(hs, hd, ids, ids)           # warm the pages
-    reps, t0 = 0, time.perf_counter()
-    while True:
-        orc.copy(hs, hd, ids, ids)
-        reps += 1
-        el = time.perf_counter() - t0
-        if el >= seconds:
-            break
-    moved = reps * 2 * n * shape.num_layers * 2 * src.tile_bytes
-    return {"value": round(moved / el / 1e9, 2), "unit": "GB/s", "cores": 1, "kind": "oracle",
+    per_pair = 2 * shape.num_layers * 2 * src.tile_bytes
+
+    def timed(chunk, budget):
+        reps, t0 = 0, time.perf_counter()
+        while True:
+            orc.copy(hs, hd, chunk, chunk)
+            reps += 1
+            el = time.perf_counter() - t0
+            if el >= budget:
+                return reps, el
+
+    # one thread
+    reps1, el1 = timed(ids, 0.4 * seconds)
+    single = reps1 * n * per_pair / el1 / 1e9
+    # every core of the process's CPU share (at most 16), each thread on its
+    # own slice of the pairs; the C oracle runs outside the interpreter lock
+    threads = max(1, min(16, len(os.sched_getaffinity(0)), n))
+    chunks = np.array_split(ids, threads)
+    budget = max(1.0, 2.0 * seconds / threads)     # about 2 x seconds of CPU work over all threads
+    from concurrent.futures import ThreadPoolExecutor
+    t0 = time.perf_counter()
+    with ThreadPoolExecutor(max_workers=threads) as ex:
+        res = list(ex.map(lambda c: (timed(c, budget), len(c)), chunks))
+    wall = time.perf_counter() - t0
+    moved = sum(r * k * per_pair for (r, _), k in res)
+    multi = moved / wall / 1e9
+    model = ""
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                model = line.split(":", 1)[1].strip()
+                break
+    except OSError:
+        pass
+    return {"value": round(multi, 2), "unit": "GB/s", "cores": threads, "kind": "oracle",
             "sample": f"{n} of the {stage1.blocks} stage-1 block pairs (all {shape.num_layers} layers, "
-                      f"K and V, {n * shape.num_layers * 2} tiles of {src.tile_bytes} B) copied {reps} times "
-                      f"from host snapshots, {el:.1f} s, one thread"}
+                      f"K and V, {n * shape.num_layers * 2} tiles of {src.tile_bytes} B) copied from host "
+                      f"snapshots by the oracle's per-tile memcpy: {threads} threads on disjoint slices for "
+                      f"{wall:.1f} s",
+            "single_thread": {"value": round(single, 2), "unit": "GB/s", "cores": 1, "seconds": round(el1, 1),
+                              "reps": reps1},
+            "cpu_model": model}
 
 
 def downtime_sweep(reps):
@@ -329,7 +379,7 @@ def downtime_sweep(reps):
     return out
 
 
-def batched_section(reps=10, host_reps=3, chunk_pairs=64):
+def batched_section(reps=20, host_reps=3, chunk_pairs=64):
     """64 requests migrated in one llmig_stage call; and the same pairs
     through pinned host memory (pack -> host -> unpack, chunked, two buffers)."""
     import torch
@@ -357,6 +407,7 @@ def batched_section(reps=10, host_reps=3, chunk_pairs=64):
     us = statistics.median(times)
     out = {"workload": su.workload.name, "requests": len(su.tables), "pairs": int(len(ms)),
            "pool_blocks": shape.num_blocks, "bytes": nbytes, "stage_us_median": round(us, 1),
+           "stage_us": spread(times),
            "GBps": round(nbytes / (us * 1e-6) / 1e9, 1),
            "lengths": {"min": int(min(su.lengths)), "median": float(statistics.median(su.lengths)),
                        "max": int(max(su.lengths)), "tokens": int(sum(su.lengths))}}
@@ -383,7 +434,7 @@ def batched_section(reps=10, host_reps=3, chunk_pairs=64):
     return out
 
 
-def xlayout_section(reps=10):
+def xlayout_section(reps=20):
     """Stage 1 of the LLaMA-7B migration (512 blocks, 4 GiB each way) between
     pools of different intra-tile layouts: the same tensors registered under
     several layouts, timed per layout pair with events on the stage's stream."""
@@ -428,7 +479,7 @@ def xlayout_section(reps=10):
         us = statistics.median(times)
         gbs = nbytes / (us * 1e-6) / 1e9
         out["cases"].append({"src": "/".join(names[x] for x in sl), "dst": "/".join(names[x] for x in dl),
-                             "stage_us_median": round(us, 1), "GBps": round(gbs, 1),
+                             "stage_us_median": round(us, 1), "stage_us": spread(times), "GBps": round(gbs, 1),
                              "hbm_frac": round(gbs / HBM_PEAK_GBS, 3)})
         log("cross-layout", out["cases"][-1])
         src.close()
