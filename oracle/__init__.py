@@ -147,6 +147,10 @@ class Oracle:
         lib.oracle_copy_layout.argtypes = [_pp, _pp, _i32p, _pp, _pp, _i32p, ctypes.c_int32, ctypes.c_int32,
                                            ctypes.c_int32, ctypes.c_int32, ctypes.c_int32, _i32p, _i32p,
                                            ctypes.c_int64]
+        lib.oracle_unpack_layout.restype = None
+        lib.oracle_unpack_layout.argtypes = [_pp, _pp, _i32p, _i32p, ctypes.c_int32, ctypes.c_int32,
+                                             ctypes.c_int32, ctypes.c_int32, ctypes.c_int32, _i32p,
+                                             ctypes.c_int64, ctypes.c_void_p]
         lib.oracle_write_tokens_layout.restype = None
         lib.oracle_write_tokens_layout.argtypes = [_pp, _pp, _i32p, ctypes.c_int32, ctypes.c_int32,
                                                    ctypes.c_int32, ctypes.c_int32, ctypes.c_int32, _i32p,
@@ -278,6 +282,25 @@ class Oracle:
         self.lib.oracle_copy_layout(sk, sv, sl.ctypes.data_as(_i32p), dk, dv, dl.ctypes.data_as(_i32p),
                                     src.num_layers, src.block_size, heads, head_dim, elem_bytes,
                                     ms.ctypes.data_as(_i32p), md.ctypes.data_as(_i32p), len(ms))
+
+    def unpack_layout(self, pool: HostPool, pool_layouts, blocks, staging: np.ndarray, staging_layouts,
+                      heads: int, head_dim: int, elem_bytes: int) -> None:
+        """Scatter a staging buffer whose tiles follow ``staging_layouts``
+        into the listed blocks of a pool whose tiles follow ``pool_layouts``."""
+        self._geometry(pool, heads, head_dim, elem_bytes)
+        b = _i32(blocks)
+        if len(b):
+            assert b.min() >= 0 and b.max() < pool.num_blocks
+        staging = np.ascontiguousarray(staging, dtype=np.uint8)
+        assert staging.size >= pool.num_layers * 2 * len(b) * pool.tile_bytes
+        pl, sl = _i32(pool_layouts), _i32(staging_layouts)
+        assert len(pl) == 2 and len(sl) == 2
+        for lay in list(pl) + list(sl):
+            assert self.layout_offset(int(lay), 0, 0, 0, pool.block_size, heads, head_dim, elem_bytes) >= 0
+        k, v = pool._ptrs()
+        self.lib.oracle_unpack_layout(k, v, pl.ctypes.data_as(_i32p), sl.ctypes.data_as(_i32p), pool.num_layers,
+                                      pool.block_size, heads, head_dim, elem_bytes, b.ctypes.data_as(_i32p),
+                                      len(b), staging.ctypes.data)
 
     def write_tokens_layout(self, pool: HostPool, layouts, table, from_tok: int, data: np.ndarray,
                             heads: int, head_dim: int, elem_bytes: int) -> None:

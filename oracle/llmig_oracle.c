@@ -490,3 +490,33 @@ int64_t oracle_first_token_mismatch_layout(uint8_t *const *a_k, uint8_t *const *
     }
     return -1;
 }
+
+/* Block fusion's receiving side between engines of different layouts: the
+ * staging buffer (laid out as oracle_pack writes it) holds tiles whose
+ * elements follow staging_layouts (K, V); every element (t, h, dim) of
+ * slot ((l * 2 + kv) * n + i) lands in tile (l, kv) of pool block
+ * blocks[i] where the pool's layouts put it. */
+void oracle_unpack_layout(uint8_t *const *pool_k, uint8_t *const *pool_v, const int32_t *pool_layouts,
+                          const int32_t *staging_layouts, int32_t num_layers, int32_t bs, int32_t heads,
+                          int32_t head_dim, int32_t elem_bytes, const int32_t *blocks, int64_t n,
+                          const uint8_t *staging)
+{
+    int64_t tile_bytes = (int64_t)bs * heads * head_dim * elem_bytes;
+    for (int32_t l = 0; l < num_layers; l++) {
+        for (int kv = 0; kv < 2; kv++) {
+            uint8_t *const *pool = (kv == 0) ? pool_k : pool_v;
+            for (int64_t i = 0; i < n; i++) {
+                const uint8_t *s = staging + (((int64_t)l * 2 + kv) * n + i) * tile_bytes;
+                uint8_t *d = pool[l] + (int64_t)blocks[i] * tile_bytes;
+                for (int64_t t = 0; t < bs; t++)
+                    for (int64_t h = 0; h < heads; h++)
+                        for (int64_t e = 0; e < head_dim; e++)
+                            memcpy(d + oracle_layout_offset(pool_layouts[kv], t, h, e, bs, heads,
+                                                            head_dim, elem_bytes),
+                                   s + oracle_layout_offset(staging_layouts[kv], t, h, e, bs, heads,
+                                                            head_dim, elem_bytes),
+                                   (size_t)elem_bytes);
+            }
+        }
+    }
+}

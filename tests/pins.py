@@ -34,7 +34,9 @@ What pins what:
                elements; offsets are a bijection onto the tile; conversions
                round-trip and compose; same-layout conversion is the byte
                copy; appends and token identity read through numpy's view;
-               a cross-layout multi-stage replay keeps every token.
+               a cross-layout multi-stage replay keeps every token; a
+               converting unpack equals the plain unpack for equal layouts,
+               the converting stage copy after a pack, and numpy's view.
 """
 from __future__ import annotations
 
@@ -613,6 +615,37 @@ def pin_xlayout_appends_and_identity(orc):
     logical[5, 0, 0] ^= 1                                   # token 29: beyond the length
     arr[:] = _arrange(logical, dl[0], e)
     assert orc.first_token_mismatch_layout(src, sl, table, c, dl, tb, length, heads, dim, e) == -1
+
+
+def pin_xlayout_unpack(orc):
+    rng = np.random.default_rng(47)
+    bs, heads, dim, e, num_layers = 8, 2, 16, 2, 2
+    slot = heads * dim * e
+    src = _random_pool(rng, num_layers, 9, bs, slot)
+    blocks_src = np.array([7, 2, 5, 0], np.int32)
+    blocks_dst = np.array([1, 6, 3, 8], np.int32)
+    for sl, dl in (((HCNX, HDN), (NHD, NHD)), ((NHD, HND), (HDN, HCNX)), ((HND, HND), (HND, HND))):
+        staging = orc.pack(src, blocks_src)
+        # staging layouts equal to the pool's: exactly the plain unpack
+        a = _random_pool(rng, num_layers, 10, bs, slot)
+        b = a.copy()
+        orc.unpack_layout(a, dl, blocks_dst, staging, dl, heads, dim, e)
+        orc.unpack(b, blocks_dst, staging)
+        assert a.equals(b)
+        # pack in one layout, unpack into another == the converting stage copy
+        c = _random_pool(rng, num_layers, 10, bs, slot)
+        d = c.copy()
+        orc.unpack_layout(c, dl, blocks_dst, staging, sl, heads, dim, e)
+        orc.copy_layout(src, sl, d, dl, blocks_src, blocks_dst, heads, dim, e)
+        assert c.equals(d), (sl, dl)
+    # a staging tile arranged by numpy in HDN lands as the NHD (logical) image
+    logical = (np.arange(bs * heads * dim) * 7 % 65521).astype(np.uint16).reshape(bs, heads, dim)
+    one = HostPool.zeros(1, 2, bs, slot)
+    staging = np.concatenate([_arrange(logical, HDN, e), _arrange(logical[::-1].copy(), HCNX, e)])
+    orc.unpack_layout(one, (NHD, NHD), [1], staging, (HDN, HCNX), heads, dim, e)
+    assert np.array_equal(one.k[0][1], logical.view(np.uint8).reshape(-1))
+    assert np.array_equal(one.v[0][1], logical[::-1].copy().view(np.uint8).reshape(-1))
+    assert not one.k[0][0].any()
 
 
 def pin_xlayout_multistage_replay(orc):

@@ -66,6 +66,10 @@ MUTANTS = [
      "oracle_layout_offset(layouts[kv], t / bs, h, e,", 0),
     ("mismatch_layout_b_read_as_a", "tb + oracle_layout_offset(b_layouts[kv]",
      "tb + oracle_layout_offset(a_layouts[kv]", 0),
+    ("unpack_layout_reads_pool_layout", "s + oracle_layout_offset(staging_layouts[kv]",
+     "s + oracle_layout_offset(pool_layouts[kv]", 0),
+    ("unpack_layout_slot_order", "const uint8_t *s = staging + (((int64_t)l * 2 + kv) * n + i) * tile_bytes;",
+     "const uint8_t *s = staging + ((i * 2 + kv) * num_layers + l) * tile_bytes;", 0),
 ]
 
 RUNNER = r"""
