@@ -437,13 +437,14 @@ def batched_section(reps=20, host_reps=3, chunk_pairs=64):
 def xlayout_section(reps=20):
     """Stage 1 of the LLaMA-7B migration (512 blocks, 4 GiB each way) between
     pools of different intra-tile layouts: the same tensors registered under
-    several layouts, timed per layout pair with events on the stage's stream."""
+    several layouts, timed per layout pair with events on the stage's stream;
+    then the same blocks unpacked from device staging with the conversion."""
     import torch
 
     from paper_2406_03243_amd import harness, scenarios
     from paper_2406_03243_amd import workloads as wl
-    from paper_2406_03243_amd.llmig import (LAYOUT_HCNX, LAYOUT_HDN, LAYOUT_HND, LAYOUT_NHD, Pool,
-                                            llmig_stage)
+    from paper_2406_03243_amd.llmig import (LAYOUT_HCNX, LAYOUT_HDN, LAYOUT_HND, LAYOUT_NHD, Pool, llmig_pack,
+                                            llmig_stage, llmig_unpack_layout)
 
     w = wl.LLAMA7B
     shape = w.shape
@@ -484,7 +485,33 @@ def xlayout_section(reps=20):
         log("cross-layout", out["cases"][-1])
         src.close()
         dst.close()
-    del sk, sv, dk, dv
+    # the receiving side of block fusion across engines: stage 1 packed from
+    # the token-major pool into device staging, then scattered into the
+    # vLLM-layout pool with the conversion on the way in (timed alone)
+    src = Pool(sk, sv, layouts=(LAYOUT_NHD, LAYOUT_NHD))
+    dst = Pool(dk, dv, layouts=(LAYOUT_HCNX, LAYOUT_HDN))
+    staging = torch.empty(n * shape.num_layers * 2 * src.tile_bytes, dtype=torch.uint8, device="cuda")
+    llmig_pack(src, ms, staging, stream=mig)
+    for _ in range(3):
+        llmig_unpack_layout(dst, md, staging, src.layouts, stream=mig)
+    torch.cuda.synchronize()
+    times = []
+    for _ in range(reps):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(mig)
+        llmig_unpack_layout(dst, md, staging, src.layouts, stream=mig)
+        e1.record(mig)
+        torch.cuda.synchronize()
+        times.append(e0.elapsed_time(e1) * 1e3)
+    us = statistics.median(times)
+    gbs = nbytes / (us * 1e-6) / 1e9
+    out["unpack_converting"] = {"staging": "NHD/NHD (device)", "dst": "HCNX/HDN", "stage_us_median": round(us, 1),
+                                "stage_us": spread(times), "GBps": round(gbs, 1),
+                                "hbm_frac": round(gbs / HBM_PEAK_GBS, 3)}
+    log("cross-layout unpack", out["unpack_converting"])
+    src.close()
+    dst.close()
+    del sk, sv, dk, dv, staging
     return out
 
 

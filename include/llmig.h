@@ -188,6 +188,20 @@ int llmig_pack(const llmig_pool *src, const int32_t *blocks, int64_t n, int map_
 int llmig_unpack(const llmig_pool *dst, const int32_t *blocks, int64_t n, int map_on_device,
                  const void *staging, int64_t staging_bytes, void *stream);
 
+/* Block fusion, receiving side between engines of different layouts: as
+ * llmig_unpack, but the staging tiles hold their elements in the layouts
+ * staging_k_layout / staging_v_layout (those of the pool that packed them)
+ * and every element lands where dst's own layouts put it (see
+ * LLMIG_LAYOUT_*).  The receiver converts, so a sender ships its tiles
+ * untouched with its two layout codes.  Staging layouts equal to dst's make
+ * it llmig_unpack.  Converting needs the conditions of a cross-layout
+ * llmig_stage (elem_bytes == 2, head_dim % 8 == 0, block_size % 8 == 0 when
+ * a side is HDN, block_size * head_dim * 2 <= 8192); else LLMIG_EINVAL, as
+ * for an unknown layout code.  Other arguments and errors as llmig_unpack. */
+int llmig_unpack_layout(const llmig_pool *dst, const int32_t *blocks, int64_t n, int map_on_device,
+                        const void *staging, int64_t staging_bytes, int32_t staging_k_layout,
+                        int32_t staging_v_layout, void *stream);
+
 /* Stand-in for decoding's KV write (§4.2: every iteration appends its
  * token's K and V and leaves earlier ones unchanged): writes tokens
  * [from_tok, from_tok + n_tok) of a request into `pool` through its host

@@ -33,6 +33,8 @@
 //  * Block ids, layouts and base addresses are wavefront-uniform and come
 //    from the kernel arguments or scalar loads; ids of up to kInlinePairs
 //    pairs travel inline, as in the same-layout copy.
+//  * The source may also be a staging buffer laid out as llmig_pack writes
+//    it (the receiving side of block fusion, §5, converting as it scatters).
 #pragma once
 
 #include <algorithm>
@@ -47,6 +49,7 @@ constexpr int kMaxSlabChunksPerLane = 8;            // slabs of up to 8 KiB
 struct ConvertArgs {
     const uint64_t *src_tab;
     const uint64_t *dst_tab;
+    const uint8_t *src_lin;     // staging buffer [L][2][lin_pairs][tile] (null: source is a pool)
     const int32_t *src_ids_dev; // device id lists (null when the ids are inline)
     const int32_t *dst_ids_dev;
     uint64_t magic_row;         // ceil(2^32 / row_chunks)
@@ -60,6 +63,8 @@ struct ConvertArgs {
     uint32_t t_chunks;          // block_size / 8: chunks of one dim's tokens (HDN)
     uint32_t chunks;            // chunks of one head slab
     uint32_t units;             // wave items: pairs * 2 * num_layers * heads
+    uint32_t lin_first;         // this launch's first pair within the whole call
+    uint32_t lin_pairs;         // pairs in the whole call (plane stride of the staging buffer)
     int32_t layouts[4];         // source K, source V, destination K, destination V
     int32_t src_ids[kInlinePairs];
     int32_t dst_ids[kInlinePairs];
@@ -121,10 +126,15 @@ __global__ void __launch_bounds__(kThreads) convert_tiles(const ConvertArgs a)
         const uint32_t layer = plane >> 1, kv = plane & 1u;
         const int32_t sl = a.layouts[kv], dl = a.layouts[2 + kv];
 
-        const int32_t sid = INLINE_IDS ? a.src_ids[i] : id_entry(a.src_ids_dev, i);
+        const uint8_t *s;
+        if (a.src_lin) {
+            s = a.src_lin + (static_cast<uint64_t>(plane) * a.lin_pairs + a.lin_first + i) * a.tile_bytes;
+        } else {
+            const int32_t sid = INLINE_IDS ? a.src_ids[i] : id_entry(a.src_ids_dev, i);
+            s = reinterpret_cast<const uint8_t *>(table_entry(a.src_tab, kv * a.num_layers + layer)) +
+                static_cast<uint64_t>(uniform(static_cast<uint32_t>(sid))) * a.tile_bytes;
+        }
         const int32_t did = INLINE_IDS ? a.dst_ids[i] : id_entry(a.dst_ids_dev, i);
-        const uint8_t *s = reinterpret_cast<const uint8_t *>(table_entry(a.src_tab, kv * a.num_layers + layer)) +
-                           static_cast<uint64_t>(uniform(static_cast<uint32_t>(sid))) * a.tile_bytes;
         uint8_t *d = reinterpret_cast<uint8_t *>(table_entry(a.dst_tab, kv * a.num_layers + layer)) +
                      static_cast<uint64_t>(uniform(static_cast<uint32_t>(did))) * a.tile_bytes;
 
@@ -224,9 +234,10 @@ int convert_chunks_per_lane(uint32_t chunks)
     return n;
 }
 
-// Launches the conversion of n pairs.  The caller has checked that the
-// geometry is supported (16-bit elements, head_dim % 8 == 0, block_size % 8
-// == 0 when a side is HDN, slabs of at most 8 KiB).
+// Launches the conversion of n pairs (src_ids null: the source is the staging
+// buffer a.src_lin, one tile per pair and plane).  The caller has checked
+// that the geometry is supported (16-bit elements, head_dim % 8 == 0,
+// block_size % 8 == 0 when a side is HDN, slabs of at most 8 KiB).
 int launch_convert(ConvertArgs a, const int32_t *src_ids, const int32_t *dst_ids, int64_t n, bool ids_on_device,
                    hipStream_t stream, uint32_t max_workgroups)
 {
@@ -242,14 +253,17 @@ int launch_convert(ConvertArgs a, const int32_t *src_ids, const int32_t *dst_ids
     if (per_launch == 0)
         return LLMIG_EINVAL;
     const void *fn = ids_on_device ? convert_kernel_n<false>(per_lane) : convert_kernel_n<true>(per_lane);
+    a.lin_pairs = static_cast<uint32_t>(n);
     for (int64_t first = 0; first < n; first += static_cast<int64_t>(per_launch)) {
         const uint32_t m = static_cast<uint32_t>(std::min<int64_t>(n - first, per_launch));
         a.units = static_cast<uint32_t>(m * units_per_pair);
+        a.lin_first = static_cast<uint32_t>(first);
         if (ids_on_device) {
-            a.src_ids_dev = src_ids + first;
+            a.src_ids_dev = src_ids ? src_ids + first : nullptr;
             a.dst_ids_dev = dst_ids + first;
         } else {
-            std::memcpy(a.src_ids, src_ids + first, m * sizeof(int32_t));
+            if (src_ids)
+                std::memcpy(a.src_ids, src_ids + first, m * sizeof(int32_t));
             std::memcpy(a.dst_ids, dst_ids + first, m * sizeof(int32_t));
         }
         void *args[] = {&a};

@@ -249,24 +249,42 @@ bool same_layouts(const llmig_pool *src, const llmig_pool *dst)
     return src->layouts[0] == dst->layouts[0] && src->layouts[1] == dst->layouts[1];
 }
 
-// Whether a stage between pools of these (equal) geometries and these
-// layouts is supported by the conversion kernel.
-bool conversion_supported(const llmig_pool *src, const llmig_pool *dst)
+// Whether the conversion kernel supports a pool of this geometry converting
+// from (or to) tiles in layouts other[0] (K) and other[1] (V).
+bool conversion_supported(const llmig_pool *pool, const int32_t *other)
 {
-    if (src->elem_bytes != 2 || src->head_dim % 8 != 0)
+    if (pool->elem_bytes != 2 || pool->head_dim % 8 != 0)
         return false;
-    const bool hdn = src->layouts[0] == LLMIG_LAYOUT_HDN || src->layouts[1] == LLMIG_LAYOUT_HDN ||
-                     dst->layouts[0] == LLMIG_LAYOUT_HDN || dst->layouts[1] == LLMIG_LAYOUT_HDN;
-    if (hdn && src->block_size % 8 != 0)
+    const bool hdn = pool->layouts[0] == LLMIG_LAYOUT_HDN || pool->layouts[1] == LLMIG_LAYOUT_HDN ||
+                     other[0] == LLMIG_LAYOUT_HDN || other[1] == LLMIG_LAYOUT_HDN;
+    if (hdn && pool->block_size % 8 != 0)
         return false;
-    const int64_t chunks = static_cast<int64_t>(src->block_size) * src->head_dim / 8;
+    const int64_t chunks = static_cast<int64_t>(pool->block_size) * pool->head_dim / 8;
     return chunks <= 64 * kMaxSlabChunksPerLane;
+}
+
+ConvertArgs convert_args(const llmig_pool *pool, const int32_t *src_layouts, const int32_t *dst_layouts)
+{
+    ConvertArgs c;
+    std::memset(&c, 0, sizeof(c));
+    c.tile_bytes = static_cast<uint32_t>(pool->tile_bytes);
+    c.num_layers = static_cast<uint32_t>(pool->num_layers);
+    c.heads = static_cast<uint32_t>(pool->num_kv_heads);
+    c.block_size = static_cast<uint32_t>(pool->block_size);
+    c.row_chunks = static_cast<uint32_t>(pool->head_dim / 8);
+    c.t_chunks = static_cast<uint32_t>(pool->block_size / 8);
+    c.chunks = static_cast<uint32_t>(pool->block_size * pool->head_dim / 8);
+    c.layouts[0] = src_layouts[0];
+    c.layouts[1] = src_layouts[1];
+    c.layouts[2] = dst_layouts[0];
+    c.layouts[3] = dst_layouts[1];
+    return c;
 }
 
 bool pools_compatible(const llmig_pool *src, const llmig_pool *dst)
 {
     return same_geometry(src, dst) && src->device == dst->device && !pools_overlap(src, dst) &&
-           (same_layouts(src, dst) || conversion_supported(src, dst));
+           (same_layouts(src, dst) || conversion_supported(src, dst->layouts));
 }
 
 int check_pair_ids(const llmig_pool *src, const llmig_pool *dst, const int32_t *ms, const int32_t *md, int64_t n)
@@ -279,21 +297,9 @@ int launch_stage(const llmig_pool *src, const llmig_pool *dst, const int32_t *ms
                  bool ids_on_device, hipStream_t stream, uint32_t max_workgroups = 0)
 {
     if (!same_layouts(src, dst)) {
-        ConvertArgs c;
-        std::memset(&c, 0, sizeof(c));
+        ConvertArgs c = convert_args(src, src->layouts, dst->layouts);
         c.src_tab = src->d_tab;
         c.dst_tab = dst->d_tab;
-        c.tile_bytes = static_cast<uint32_t>(src->tile_bytes);
-        c.num_layers = static_cast<uint32_t>(src->num_layers);
-        c.heads = static_cast<uint32_t>(src->num_kv_heads);
-        c.block_size = static_cast<uint32_t>(src->block_size);
-        c.row_chunks = static_cast<uint32_t>(src->head_dim / 8);
-        c.t_chunks = static_cast<uint32_t>(src->block_size / 8);
-        c.chunks = static_cast<uint32_t>(src->block_size * src->head_dim / 8);
-        c.layouts[0] = src->layouts[0];
-        c.layouts[1] = src->layouts[1];
-        c.layouts[2] = dst->layouts[0];
-        c.layouts[3] = dst->layouts[1];
         return launch_convert(c, ms, md, n, ids_on_device, stream, max_workgroups);
     }
     CopyArgs a;
@@ -650,6 +656,33 @@ int llmig_unpack(const llmig_pool *dst, const int32_t *blocks, int64_t n, int ma
     a.num_layers = static_cast<uint32_t>(dst->num_layers);
     return launch_copy<kLinear, kPool>(a, nullptr, blocks, n, map_on_device != 0,
                                        static_cast<hipStream_t>(stream));
+}
+
+int llmig_unpack_layout(const llmig_pool *dst, const int32_t *blocks, int64_t n, int map_on_device,
+                        const void *staging, int64_t staging_bytes, int32_t staging_k_layout,
+                        int32_t staging_v_layout, void *stream)
+{
+    const int32_t from[2] = {staging_k_layout, staging_v_layout};
+    for (int32_t layout : from)
+        if (layout < LLMIG_LAYOUT_NHD || layout > LLMIG_LAYOUT_HDN)
+            return LLMIG_EINVAL;
+    if (dst && from[0] == dst->layouts[0] && from[1] == dst->layouts[1])
+        return llmig_unpack(dst, blocks, n, map_on_device, staging, staging_bytes, stream);
+    int rc = fused_copy_checks(dst, blocks, n, map_on_device, staging, staging_bytes, true);
+    if (rc != LLMIG_OK)
+        return rc;
+    if (!conversion_supported(dst, from))
+        return LLMIG_EINVAL;
+    if (n == 0)
+        return LLMIG_OK;
+    void *lin = nullptr;
+    rc = staging_pointer(staging, &lin);
+    if (rc != LLMIG_OK)
+        return rc;
+    ConvertArgs c = convert_args(dst, from, dst->layouts);
+    c.src_lin = static_cast<const uint8_t *>(lin);
+    c.dst_tab = dst->d_tab;
+    return launch_convert(c, nullptr, blocks, n, map_on_device != 0, static_cast<hipStream_t>(stream), 0);
 }
 
 int llmig_write_tokens(const llmig_pool *pool, const int32_t *table, int64_t table_len, int64_t from_tok,

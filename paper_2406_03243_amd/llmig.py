@@ -69,6 +69,9 @@ _lib.llmig_pack.argtypes = [_vp, _vp, ctypes.c_int64, ctypes.c_int, _vp, ctypes.
 _lib.llmig_pack.restype = ctypes.c_int
 _lib.llmig_unpack.argtypes = [_vp, _vp, ctypes.c_int64, ctypes.c_int, _vp, ctypes.c_int64, _vp]
 _lib.llmig_unpack.restype = ctypes.c_int
+_lib.llmig_unpack_layout.argtypes = [_vp, _vp, ctypes.c_int64, ctypes.c_int, _vp, ctypes.c_int64, ctypes.c_int32,
+                                     ctypes.c_int32, _vp]
+_lib.llmig_unpack_layout.restype = ctypes.c_int
 _lib.llmig_write_tokens.argtypes = [_vp, _vp, ctypes.c_int64, ctypes.c_int64, ctypes.c_int64, _vp, _vp]
 _lib.llmig_write_tokens.restype = ctypes.c_int
 _lib.llmig_stream_read.argtypes = [_vp, ctypes.c_int64, ctypes.c_int32, ctypes.c_int32, _vp, ctypes.c_int64, _vp]
@@ -234,6 +237,15 @@ def llmig_unpack(dst: Pool, blocks, staging: torch.Tensor, stream=None) -> None:
     pb, n, on_dev, keep = _ids(blocks)
     ptr, nbytes = _staging(staging)
     _check(_lib.llmig_unpack(dst.handle, pb, n, on_dev, ptr, nbytes, _stream(stream)), "llmig_unpack")
+
+
+def llmig_unpack_layout(dst: Pool, blocks, staging: torch.Tensor, staging_layouts, stream=None) -> None:
+    """Scatter a buffer packed from a pool whose (K, V) layouts were
+    ``staging_layouts`` into the listed blocks, converting to dst's layouts."""
+    pb, n, on_dev, keep = _ids(blocks)
+    ptr, nbytes = _staging(staging)
+    _check(_lib.llmig_unpack_layout(dst.handle, pb, n, on_dev, ptr, nbytes, int(staging_layouts[0]),
+                                    int(staging_layouts[1]), _stream(stream)), "llmig_unpack_layout")
 
 
 def llmig_write_tokens(pool: Pool, table, from_tok: int, data: torch.Tensor, stream=None) -> None:

@@ -239,3 +239,57 @@ def test_unsupported_conversions_are_rejected():
         llmig.llmig_decode_attention(a, q, torch.zeros((1, 1), dtype=torch.int32, device="cuda"), [10], 1.0,
                                      ws, out)
     torch.cuda.synchronize()
+
+
+@pytest.mark.parametrize("where", ["device", "pinned"])
+def test_unpack_converts_between_layouts(where):
+    """Block fusion across engines: pack from a pool of one layout, unpack
+    into a pool of another, converting on the way in."""
+    shape = wl.PoolShape(2, 60, 16, 4, 128, "bf16")
+    for j, (sl, dl) in enumerate([((NHD, NHD), (HCNX, HDN)), ((HCNX, HDN), (NHD, HND)), ((HND, NHD), (HND, HDN))]):
+        say("unpack convert", where, lay_name(sl, dl))
+        seed = 8900 + j
+        src = make_pool(shape, seed, wl.SRC_VALUES, sl)
+        dst = make_pool(shape, seed, wl.DST_VALUES, dl)
+        g = wl.stream(seed, wl.EXTRA)
+        n = 37
+        ms = g.choice(60, n, replace=False).astype(np.int32)
+        md = g.choice(60, n, replace=False).astype(np.int32)
+        nbytes = n * 2 * 2 * src.tile_bytes
+        if where == "device":
+            staging = torch.empty(nbytes, dtype=torch.uint8, device="cuda")
+        else:
+            staging = torch.empty(nbytes, dtype=torch.uint8, pin_memory=True)
+        hs, hd = host_image(src), host_image(dst)
+        llmig.llmig_pack(src, ms, staging)
+        llmig.llmig_unpack_layout(dst, torch.from_numpy(md).cuda() if j == 1 else md, staging, sl)
+        torch.cuda.synchronize()
+        want = oracle.default().pack(hs, ms)
+        oracle.default().unpack_layout(hd, dl, md, want, sl, 4, 128, 2)
+        assert_same(host_image(dst), hd, "destination")
+
+
+def test_unpack_layout_errors_and_plain_case():
+    say("unpack convert errors")
+    shape = wl.PoolShape(1, 8, 12, 1, 64, "fp16")
+    k, v = harness.alloc_layers(shape)
+    pool = Pool(k, v, layouts=(NHD, NHD))
+    staging = torch.zeros(2 * 2 * pool.tile_bytes, dtype=torch.uint8, device="cuda")
+    ids = np.array([0, 1], np.int32)
+    with pytest.raises(LlmigError):                     # HDN with 12-token blocks
+        llmig.llmig_unpack_layout(pool, ids, staging, (HDN, NHD))
+    with pytest.raises(LlmigError):                     # no such layout
+        llmig.llmig_unpack_layout(pool, ids, staging, (NHD, 7))
+    with pytest.raises(LlmigError):                     # staging too small
+        llmig.llmig_unpack_layout(pool, ids, staging[:100], (HND, NHD))
+    with pytest.raises(LlmigError):                     # repeated destination
+        llmig.llmig_unpack_layout(pool, np.array([1, 1], np.int32), staging, (HND, NHD))
+    # equal layouts: the plain unpack, bytes as they are
+    data = wl.random_bytes(9000, wl.EXTRA, staging.numel())
+    staging.copy_(torch.from_numpy(data))
+    llmig.llmig_unpack_layout(pool, ids, staging, (NHD, NHD))
+    torch.cuda.synchronize()
+    got = host_image(pool)
+    t = pool.tile_bytes
+    assert np.array_equal(got.k[0][0], data[:t]) and np.array_equal(got.k[0][1], data[t:2 * t])
+    assert np.array_equal(got.v[0][0], data[2 * t:3 * t]) and np.array_equal(got.v[0][1], data[3 * t:])
