@@ -277,8 +277,9 @@ int llmig_migration_stage(llmig_migration *m, const llmig_pool *src, const llmig
  * resident, which leaves CUs and HBM bandwidth to the decode work running
  * beside the migration at the cost of a slower copy: the lever for the
  * paper's goal of near-zero overhead on running requests (§6.2), since
- * stream priorities do not preempt running workgroups.  LLMIG_EINVAL for a
- * negative value. */
+ * stream priorities do not preempt running workgroups.  The same-layout
+ * copy's workgroups hold four wavefronts, the cross-layout copy's two.
+ * LLMIG_EINVAL for a negative value. */
 int llmig_migration_set_max_workgroups(llmig_migration *m, int32_t max_workgroups);
 
 /* Aborts (ACTIVE or FINISHED): writes every reserved destination block to
