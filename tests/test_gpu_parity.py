@@ -356,3 +356,57 @@ def test_capped_grid_multistage(cap):
     oracle.default().copy(hs, hd, table[:len(got)], got)
     assert_same(host_image(dst), hd, "destination")
     assert oracle.default().first_token_mismatch(hs, table, host_image(dst), got, 1709) == -1
+
+
+def test_concurrent_stages_from_threads():
+    """Four host threads migrate from one shared source pool into four
+    destination pools at once, each on its own stream, with the same and
+    with different layouts: the calls are independent (no shared state but
+    the immutable pool handles)."""
+    import threading
+    say("concurrent stages, 4 threads")
+    shape = wl.PoolShape(2, 200, 16, 4, 64, "fp16")
+    seed = 9100
+    src = make_pool(shape, seed, wl.SRC_VALUES, random_bytes=True)
+    hs = host_image(src)
+    layouts = [(0, 0), (0, 0), (2, 3), (1, 0)]
+    dsts = []
+    for j, lay in enumerate(layouts):
+        k, v = harness.alloc_layers(shape)
+        total = sum(t.numel() * t.element_size() for t in k + v)
+        harness.fill_bytes_from_host(k + v, wl.random_bytes(seed, wl.DST_VALUES, total, sub=j))
+        dsts.append(Pool(k, v, layouts=lay))
+    before = [host_image(d) for d in dsts]
+    plans = []
+    for j in range(len(dsts)):
+        g = wl.stream(seed, wl.EXTRA, j)
+        plans.append([(g.choice(200, 24, replace=False).astype(np.int32),
+                       g.choice(200, 24, replace=False).astype(np.int32)) for _ in range(12)])
+    errors = []
+
+    def worker(j):
+        try:
+            st = torch.cuda.Stream()
+            for ms, md in plans[j]:
+                llmig.llmig_stage(src, dsts[j], ms, md, stream=st)
+            st.synchronize()
+        except Exception as e:          # reported below, on the main thread
+            errors.append((j, e))
+
+    threads = [threading.Thread(target=worker, args=(j,)) for j in range(len(dsts))]
+    for t in threads:
+        t.start()
+    for t in threads:
+        t.join()
+    torch.cuda.synchronize()
+    assert not errors, errors
+    orc = oracle.default()
+    for j, d in enumerate(dsts):
+        want = before[j]
+        for ms, md in plans[j]:
+            if layouts[j] == (0, 0):
+                orc.copy(hs, want, ms, md)
+            else:
+                orc.copy_layout(hs, (0, 0), want, layouts[j], ms, md, 4, 64, 2)
+        assert_same(host_image(d), want, f"destination {j}")
+    assert_same(host_image(src), hs, "source")

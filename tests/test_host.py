@@ -119,6 +119,9 @@ def test_enqueue_calls_reject_bad_arguments_without_gpu():
     assert lib.llmig_stage(None, None, None, None, 0, 0, None) == llmig.LLMIG_EINVAL
     assert lib.llmig_pack(None, None, 0, 0, None, 0, None) == llmig.LLMIG_EINVAL
     assert lib.llmig_unpack(None, None, 0, 0, None, 0, None) == llmig.LLMIG_EINVAL
+    assert lib.llmig_unpack_layout(None, None, 0, 0, None, 0, 0, 0, None) == llmig.LLMIG_EINVAL
+    assert lib.llmig_unpack_layout(None, None, 0, 0, None, 0, 1, 3, None) == llmig.LLMIG_EINVAL
+    assert lib.llmig_unpack_layout(None, None, 0, 0, None, 0, 4, 0, None) == llmig.LLMIG_EINVAL
     assert lib.llmig_write_tokens(None, None, 0, 0, 0, None, None) == llmig.LLMIG_EINVAL
     assert lib.llmig_pool_create(None, None) == llmig.LLMIG_EINVAL
     out = ctypes.c_void_p(1)
