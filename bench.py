@@ -123,7 +123,7 @@ def main():
     if not os.path.exists(LIBRARY):
         import __graft_entry__
         __graft_entry__.build()
-    from paper_2406_03243_amd import migrate, scenarios
+    from paper_2406_03243_amd import harness, migrate, scenarios
 
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
@@ -134,7 +134,7 @@ def main():
     table, free, counts, appends = su.tables[0], su.free, su.counts, su.appends
     log("allocated", w.name, shape)
     initial = su.lengths[0]
-    mig, dec = torch.cuda.Stream(device=dev), torch.cuda.Stream(device=dev)
+    mig, dec = harness.concurrent_streams(2)
     torch.cuda.synchronize()
 
     def step():
@@ -384,7 +384,7 @@ def batched_section(reps=20, host_reps=3, chunk_pairs=64):
     through pinned host memory (pack -> host -> unpack, chunked, two buffers)."""
     import torch
 
-    from paper_2406_03243_amd import migrate, scenarios
+    from paper_2406_03243_amd import harness, migrate, scenarios
     from paper_2406_03243_amd.llmig import llmig_stage
 
     su = scenarios.batched()
@@ -415,7 +415,7 @@ def batched_section(reps=20, host_reps=3, chunk_pairs=64):
     bufs = [torch.empty(chunk_bytes, dtype=torch.uint8, pin_memory=True) for _ in range(2)]
     dev_bufs = [(torch.empty(chunk_bytes, dtype=torch.uint8, device="cuda"),
                  torch.empty(chunk_bytes, dtype=torch.uint8, device="cuda")) for _ in range(2)]
-    ps, us_ = torch.cuda.Stream(), torch.cuda.Stream()
+    ps, us_ = harness.concurrent_streams(2)
     one_way = len(ms) * shape.num_layers * 2 * src.tile_bytes
     out["host_staged"] = {"chunk_pairs": chunk_pairs, "bytes_each_way": one_way,
                           "bound": "PCIe Gen5 x16, ~64 GB/s per direction"}
@@ -521,7 +521,7 @@ def load_section(reps=3, reader_passes=3, step_ms=20.0, caps=(0, 256, 64)):
     the migration's copy grid (0: uncapped)."""
     import torch
 
-    from paper_2406_03243_amd import migrate, scenarios
+    from paper_2406_03243_amd import harness, migrate, scenarios
     from paper_2406_03243_amd.llmig import llmig_stream_read
 
     su = scenarios.gqa_long()
@@ -531,7 +531,7 @@ def load_section(reps=3, reader_passes=3, step_ms=20.0, caps=(0, 256, 64)):
     cus = torch.cuda.get_device_properties(0).multi_processor_count
     wgs = cus * 4
     sink = torch.empty(wgs * 256, dtype=torch.int64, device="cuda")
-    rd, mig, dec = torch.cuda.Stream(), torch.cuda.Stream(), torch.cuda.Stream()
+    rd, mig, dec = harness.concurrent_streams(3)
     length = su.lengths[0]
     read_bytes = reader_passes * region.numel() * region.element_size()
 
@@ -595,7 +595,7 @@ def decode_overhead(su, caps, step_ms, steps=14, reps=5):
     migration running beside it (Llumnix §6.2 reports at most 1% slowdown)."""
     import torch
 
-    from paper_2406_03243_amd import migrate, scenarios
+    from paper_2406_03243_amd import harness, migrate, scenarios
     from paper_2406_03243_amd.llmig import decode_workspace_bytes, llmig_decode_attention
 
     shape, src, dst, table, free = su.shape, su.src, su.dst, su.tables[0], su.free
@@ -605,7 +605,7 @@ def decode_overhead(su, caps, step_ms, steps=14, reps=5):
     ws = torch.empty(decode_workspace_bytes(ctx, shape.num_layers, q.shape[2], shape.head_dim),
                      dtype=torch.uint8, device="cuda")
     scale = 1.0 / math.sqrt(shape.head_dim)
-    at, mig, dec = torch.cuda.Stream(), torch.cuda.Stream(), torch.cuda.Stream()
+    at, mig, dec = harness.concurrent_streams(3)
     kv_bytes = sum(ctx) * shape.num_layers * 2 * shape.kv_heads * shape.head_dim * shape.elem_bytes
 
     def decode_steps(n):

@@ -62,3 +62,47 @@ def snapshot_blocks(tensors, ids):
     """Host copies of the listed blocks of every tensor, uint8 [len(ids), tile_bytes]."""
     idx = torch.as_tensor(np.asarray(ids, dtype=np.int64), device=tensors[0].device)
     return [tile_view(t).index_select(0, idx).cpu().numpy() for t in tensors]
+
+
+def concurrent_streams(n: int, candidates: int = 16, probe_bytes: int = 4 * 10**9):
+    """``n`` torch streams whose kernels run side by side.
+
+    Streams share the GPU's few hardware queues, and the kernels of two
+    streams on one queue run one after the other, so streams meant to
+    overlap (a migration beside decoding, double-buffered copies) are chosen
+    by measurement: a stream joins the set when a short read launched on it
+    completes while a long read on each stream already chosen is still
+    running.  Raises RuntimeError when ``candidates`` fresh streams hold no
+    such set."""
+    from .llmig import llmig_stream_read
+
+    dev = torch.device("cuda", torch.cuda.current_device())
+    long_region = torch.empty(probe_bytes, dtype=torch.uint8, device=dev)
+    short_region = torch.empty(16 << 20, dtype=torch.uint8, device=dev)
+    long_region.zero_()
+    short_region.zero_()
+    sink_long = torch.empty(256 * 256, dtype=torch.int64, device=dev)
+    sink_short = torch.empty(64 * 256, dtype=torch.int64, device=dev)
+    torch.cuda.synchronize()
+
+    def overlaps(a, b) -> bool:
+        e = [torch.cuda.Event(enable_timing=True) for _ in range(3)]
+        e[0].record(a)
+        llmig_stream_read(long_region, 1, 256, sink_long, stream=a)
+        e[1].record(a)
+        llmig_stream_read(short_region, 1, 64, sink_short, stream=b)
+        e[2].record(b)
+        torch.cuda.synchronize()
+        return e[0].elapsed_time(e[2]) < 0.5 * e[0].elapsed_time(e[1])
+
+    chosen = []
+    for _ in range(candidates):
+        s = torch.cuda.Stream(device=dev)
+        if all(overlaps(c, s) and overlaps(s, c) for c in chosen):
+            chosen.append(s)
+            if len(chosen) == n:
+                break
+    del long_region, short_region, sink_long, sink_short
+    if len(chosen) < n:
+        raise RuntimeError(f"found only {len(chosen)} of {n} streams that run side by side")
+    return chosen
