@@ -183,7 +183,7 @@ def test_multistage_scheduled_small():
     free, _ = wl.free_list(seed, shape.num_blocks, 0.3)
     data = _appends(shape, seed, counts, src.slot_bytes)
     hs, hd = host_image(src), host_image(dst)
-    mig, dec = torch.cuda.Stream(), torch.cuda.Stream()
+    mig, dec = harness.concurrent_streams(2)
     m, downtime = migrate.run_scheduled(src, dst, table, free, initial,
                                         [torch.from_numpy(x).cuda() for x in data], mig, dec)
     torch.cuda.synchronize()
@@ -225,7 +225,7 @@ def test_multistage_timed_small():
     llmig.llmig_write_tokens(wa, [0], 0, torch.zeros(6 * 2 * src.slot_bytes, dtype=torch.uint8, device="cuda"))
     torch.cuda.synchronize()
     hs, hd = host_image(src), host_image(dst)
-    mig, dec = torch.cuda.Stream(), torch.cuda.Stream()
+    mig, dec = harness.concurrent_streams(2)
     # a very short simulated decode step forces several stages
     m, downtime = migrate.run_timed(src, dst, table, initial, free, torch.from_numpy(append_pool).cuda(),
                                     mig, dec, step_ms=0.005, last_stage_max_blocks=1, max_stages=6)
