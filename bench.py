@@ -91,6 +91,14 @@ def spread(us):
             "p90": round(percentile(us, 90), 2), "n": len(us)}
 
 
+def inline_launch(src_blocks: int, dst_blocks: int):
+    """(ids mode, pairs per launch) of a pool-to-pool stage with host ids:
+    16-bit packed ids, 512 pairs a launch, when both pools have at most
+    65536 blocks, else 32-bit ids, 256 a launch (mirrors the library's
+    launch configuration, for labelling only)."""
+    return (2, 512) if max(src_blocks, dst_blocks) <= 65536 else (1, 256)
+
+
 def stage_bytes(blocks, shape, tile_bytes):
     """Algorithmic bytes of a stage: every tile read once and written once."""
     return 2 * blocks * shape.num_layers * 2 * tile_bytes
@@ -134,7 +142,7 @@ def main():
     table, free, counts, appends = su.tables[0], su.free, su.counts, su.appends
     log("allocated", w.name, shape)
     initial = su.lengths[0]
-    mig, dec = harness.concurrent_streams(2)
+    (mig, dec), overlap = harness.concurrent_streams(2)
     torch.cuda.synchronize()
 
     def step():
@@ -176,16 +184,17 @@ def main():
     value = bytes_per_step / (elapsed / args.steps) / 1e9
 
     # dominant kernel: the bulk pool-to-pool copy of stage 1, launched on the
-    # migration stream; its ids travel in the kernel arguments, 256 pairs per launch
+    # migration stream; its ids travel in the kernel arguments
     s1_blocks = m0.stages[0].blocks
-    launches = math.ceil(s1_blocks / 256)
+    ids_mode, per_launch_pairs = inline_launch(src.num_blocks, dst.num_blocks)
+    launches = math.ceil(s1_blocks / per_launch_pairs)
     s1_us = [m.stages[0].gpu_us for m, _ in runs]
     s1_avg_us = statistics.fmean(s1_us)
     per_launch_bytes = stage_bytes(s1_blocks, shape, src.tile_bytes) / launches
     per_launch_us = s1_avg_us / launches
     achieved = per_launch_bytes / (per_launch_us * 1e-6) / 1e9
     downtimes = [d for _, d in runs]
-    kernel_name = "copy_tiles<0, 0, true, %d>" % bulk_span_rows(src.tile_bytes)
+    kernel_name = "copy_tiles<0, 0, %d, %d>" % (ids_mode, bulk_span_rows(src.tile_bytes))
 
     stages = []
     for i, rec in enumerate(m0.stages):
@@ -227,6 +236,7 @@ def main():
                      "launches_per_stage": launches, "bytes_per_launch": int(per_launch_bytes),
                      "avg_launch_us": round(per_launch_us, 2)},
         "stages": stages,
+        "streams_overlap": overlap,
         "final_stage_downtime_us": {"median": round(statistics.median(downtimes), 1),
                                     "min": round(min(downtimes), 1), "max": round(max(downtimes), 1)},
     }
@@ -415,10 +425,10 @@ def batched_section(reps=20, host_reps=3, chunk_pairs=64):
     bufs = [torch.empty(chunk_bytes, dtype=torch.uint8, pin_memory=True) for _ in range(2)]
     dev_bufs = [(torch.empty(chunk_bytes, dtype=torch.uint8, device="cuda"),
                  torch.empty(chunk_bytes, dtype=torch.uint8, device="cuda")) for _ in range(2)]
-    ps, us_ = harness.concurrent_streams(2)
+    (ps, us_), overlap = harness.concurrent_streams(2)
     one_way = len(ms) * shape.num_layers * 2 * src.tile_bytes
     out["host_staged"] = {"chunk_pairs": chunk_pairs, "bytes_each_way": one_way,
-                          "bound": "PCIe Gen5 x16, ~64 GB/s per direction"}
+                          "bound": "PCIe Gen5 x16, ~64 GB/s per direction", "streams_overlap": overlap}
     for mode, db in (("kernel_pcie", None), ("copy_engine", dev_bufs)):
         host_times = []
         for r in range(host_reps + 1):
@@ -531,7 +541,7 @@ def load_section(reps=3, reader_passes=3, step_ms=20.0, caps=(0, 256, 64)):
     cus = torch.cuda.get_device_properties(0).multi_processor_count
     wgs = cus * 4
     sink = torch.empty(wgs * 256, dtype=torch.int64, device="cuda")
-    rd, mig, dec = harness.concurrent_streams(3)
+    (rd, mig, dec), overlap = harness.concurrent_streams(3)
     length = su.lengths[0]
     read_bytes = reader_passes * region.numel() * region.element_size()
 
@@ -549,7 +559,7 @@ def load_section(reps=3, reader_passes=3, step_ms=20.0, caps=(0, 256, 64)):
         if r:
             alone_r.append(e[0].elapsed_time(e[1]) * 1e3)
     r_alone = statistics.median(alone_r)
-    out = {"workload": su.workload.name, "tokens": length, "reader_bytes": read_bytes,
+    out = {"workload": su.workload.name, "tokens": length, "reader_bytes": read_bytes, "streams_overlap": overlap,
            "reader_workgroups": wgs, "reader_alone_GBps": round(read_bytes / (r_alone * 1e-6) / 1e9, 1),
            "by_cap": {}}
     out["beside_decode"] = decode_overhead(su, caps, step_ms)
@@ -605,7 +615,7 @@ def decode_overhead(su, caps, step_ms, steps=14, reps=5):
     ws = torch.empty(decode_workspace_bytes(ctx, shape.num_layers, q.shape[2], shape.head_dim),
                      dtype=torch.uint8, device="cuda")
     scale = 1.0 / math.sqrt(shape.head_dim)
-    at, mig, dec = harness.concurrent_streams(3)
+    (at, mig, dec), overlap = harness.concurrent_streams(3)
     kv_bytes = sum(ctx) * shape.num_layers * 2 * shape.kv_heads * shape.head_dim * shape.elem_bytes
 
     def decode_steps(n):
@@ -623,7 +633,7 @@ def decode_overhead(su, caps, step_ms, steps=14, reps=5):
     torch.cuda.synchronize()
     alone = [evs[i].elapsed_time(evs[i + 1]) * 1e3 for i in range(steps)]
     t_alone = statistics.median(alone)
-    res = {"batch": len(ctx), "tokens": int(sum(ctx)), "kv_bytes_per_step": kv_bytes,
+    res = {"batch": len(ctx), "tokens": int(sum(ctx)), "kv_bytes_per_step": kv_bytes, "streams_overlap": overlap,
            "step_us_alone": round(t_alone, 1), "decode_GBps_alone": round(kv_bytes / (t_alone * 1e-6) / 1e9, 1),
            "by_cap": {}}
     for cap in caps:

@@ -282,6 +282,16 @@ int llmig_migration_stage(llmig_migration *m, const llmig_pool *src, const llmig
  * LLMIG_EINVAL for a negative value. */
 int llmig_migration_set_max_workgroups(llmig_migration *m, int32_t max_workgroups);
 
+/* Times the next llmig_migration_stage call on the GPU: start_event (a
+ * hipEvent_t, NULL for none) is recorded as the stage's first kernel starts
+ * and stop_event as its last kernel ends, so their interval is the stage's
+ * kernel time without the host's launch latency (events recorded on the
+ * stream around the call include it).  The events are the caller's,
+ * created with timing enabled; they apply to that one call, which records
+ * nothing if its stage is empty or fails before launching.  Host only;
+ * LLMIG_EINVAL for m == NULL. */
+int llmig_migration_set_stage_events(llmig_migration *m, void *start_event, void *stop_event);
+
 /* Aborts (ACTIVE or FINISHED): writes every reserved destination block to
  * out (capacity cap; *out_n = count) so the destination can release them,
  * and moves to ABORTED.  Copies already enqueued may still write into those

@@ -244,7 +244,7 @@ int convert_chunks_per_lane(uint32_t chunks)
 // that the geometry is supported (16-bit elements, head_dim % 8 == 0,
 // block_size % 8 == 0 when a side is HDN, slabs of at most 8 KiB).
 int launch_convert(ConvertArgs a, const int32_t *src_ids, const int32_t *dst_ids, int64_t n, bool ids_on_device,
-                   hipStream_t stream, uint32_t max_workgroups)
+                   hipStream_t stream, uint32_t max_workgroups, const LaunchEvents &ev = LaunchEvents())
 {
     const int per_lane = convert_chunks_per_lane(a.chunks);
     if (per_lane > kMaxSlabChunksPerLane)
@@ -259,7 +259,8 @@ int launch_convert(ConvertArgs a, const int32_t *src_ids, const int32_t *dst_ids
         return LLMIG_EINVAL;
     const void *fn = ids_on_device ? convert_kernel_n<false>(per_lane) : convert_kernel_n<true>(per_lane);
     a.lin_pairs = static_cast<uint32_t>(n);
-    for (int64_t first = 0; first < n; first += static_cast<int64_t>(per_launch)) {
+    const int64_t launches = (n + static_cast<int64_t>(per_launch) - 1) / static_cast<int64_t>(per_launch);
+    for (int64_t first = 0, k = 0; first < n; first += static_cast<int64_t>(per_launch), ++k) {
         const uint32_t m = static_cast<uint32_t>(std::min<int64_t>(n - first, per_launch));
         a.units = static_cast<uint32_t>(m * units_per_pair);
         a.lin_first = static_cast<uint32_t>(first);
@@ -275,7 +276,7 @@ int launch_convert(ConvertArgs a, const int32_t *src_ids, const int32_t *dst_ids
         uint32_t grid = (a.units + kConvertWaves - 1) / kConvertWaves;
         if (max_workgroups > 0)
             grid = std::min(grid, max_workgroups);
-        hipError_t e = hipLaunchKernel(fn, dim3(grid), dim3(kConvertWaves * 64), args, 0, stream);
+        hipError_t e = launch_kernel(fn, dim3(grid), dim3(kConvertWaves * 64), args, stream, ev, k, launches);
         if (e != hipSuccess)
             return hip_error(e);
     }

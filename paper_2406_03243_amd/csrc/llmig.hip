@@ -40,6 +40,7 @@ struct llmig_migration {
     int64_t copied_tok;               // tokens copied by the stages so far
     int64_t stages;
     uint32_t max_workgroups;          // 0: no cap on the copy grid
+    LaunchEvents next_events;         // events for the next stage's kernels (then cleared)
     std::vector<int32_t> reserved;    // destination blocks, in logical order
     std::vector<int32_t> plan_src;    // per-stage scratch, reused
     std::vector<int32_t> plan_dst;
@@ -294,13 +295,14 @@ int check_pair_ids(const llmig_pool *src, const llmig_pool *dst, const int32_t *
 }
 
 int launch_stage(const llmig_pool *src, const llmig_pool *dst, const int32_t *ms, const int32_t *md, int64_t n,
-                 bool ids_on_device, hipStream_t stream, uint32_t max_workgroups = 0)
+                 bool ids_on_device, hipStream_t stream, uint32_t max_workgroups = 0,
+                 const LaunchEvents &ev = LaunchEvents())
 {
     if (!same_layouts(src, dst)) {
         ConvertArgs c = convert_args(src, src->layouts, dst->layouts);
         c.src_tab = src->d_tab;
         c.dst_tab = dst->d_tab;
-        return launch_convert(c, ms, md, n, ids_on_device, stream, max_workgroups);
+        return launch_convert(c, ms, md, n, ids_on_device, stream, max_workgroups, ev);
     }
     CopyArgs a;
     std::memset(&a, 0, sizeof(a));
@@ -308,7 +310,9 @@ int launch_stage(const llmig_pool *src, const llmig_pool *dst, const int32_t *ms
     a.dst_tab = dst->d_tab;
     a.tile_bytes = static_cast<uint32_t>(src->tile_bytes);
     a.num_layers = static_cast<uint32_t>(src->num_layers);
-    return launch_copy<kPool, kPool>(a, ms, md, n, ids_on_device, stream, max_workgroups);
+    // ids are range-checked against the pools when they come from the host
+    const bool ids16 = src->num_blocks <= 65536 && dst->num_blocks <= 65536;
+    return launch_copy<kPool, kPool>(a, ms, md, n, ids_on_device, stream, max_workgroups, ids16, ev);
 }
 
 // Token range of the next stage of m for a request now holding len tokens.
@@ -485,6 +489,7 @@ int llmig_migration_create(int32_t block_size, llmig_migration **out)
     m->copied_tok = 0;
     m->stages = 0;
     m->max_workgroups = 0;
+    m->next_events = LaunchEvents();
     *out = m;
     return LLMIG_OK;
 }
@@ -522,6 +527,8 @@ int llmig_migration_stage(llmig_migration *m, const llmig_pool *src, const llmig
     if (!m || !out_n)
         return LLMIG_EINVAL;
     *out_n = 0;
+    const LaunchEvents ev = m->next_events; // this call's, whatever happens below
+    m->next_events = LaunchEvents();
     if (!src || !dst || !pools_compatible(src, dst) || src->block_size != m->block_size)
         return LLMIG_EINVAL;
     int64_t from = 0, to = 0;
@@ -556,7 +563,16 @@ int llmig_migration_stage(llmig_migration *m, const llmig_pool *src, const llmig
     if (n == 0)
         return LLMIG_OK;
     return launch_stage(src, dst, m->plan_src.data(), m->plan_dst.data(), n, false,
-                        static_cast<hipStream_t>(stream), final_stage ? 0u : m->max_workgroups);
+                        static_cast<hipStream_t>(stream), final_stage ? 0u : m->max_workgroups, ev);
+}
+
+int llmig_migration_set_stage_events(llmig_migration *m, void *start_event, void *stop_event)
+{
+    if (!m)
+        return LLMIG_EINVAL;
+    m->next_events.start = static_cast<hipEvent_t>(start_event);
+    m->next_events.stop = static_cast<hipEvent_t>(stop_event);
+    return LLMIG_OK;
 }
 
 int llmig_migration_set_max_workgroups(llmig_migration *m, int32_t max_workgroups)

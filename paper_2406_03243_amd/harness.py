@@ -65,15 +65,16 @@ def snapshot_blocks(tensors, ids):
 
 
 def concurrent_streams(n: int, candidates: int = 16, probe_bytes: int = 4 * 10**9):
-    """``n`` torch streams whose kernels run side by side.
+    """``n`` torch streams whose kernels run side by side, and whether they do.
 
     Streams share the GPU's few hardware queues, and the kernels of two
     streams on one queue run one after the other, so streams meant to
     overlap (a migration beside decoding, double-buffered copies) are chosen
     by measurement: a stream joins the set when a short read launched on it
     completes while a long read on each stream already chosen is still
-    running.  Raises RuntimeError when ``candidates`` fresh streams hold no
-    such set."""
+    running.  When ``candidates`` fresh streams hold no such set (a profiler
+    that serialises kernels, say), the set is filled with the remaining
+    candidates and the flag is False.  Returns (streams, overlap)."""
     from .llmig import llmig_stream_read
 
     dev = torch.device("cuda", torch.cuda.current_device())
@@ -95,14 +96,16 @@ def concurrent_streams(n: int, candidates: int = 16, probe_bytes: int = 4 * 10**
         torch.cuda.synchronize()
         return e[0].elapsed_time(e[2]) < 0.5 * e[0].elapsed_time(e[1])
 
-    chosen = []
+    chosen, rest = [], []
     for _ in range(candidates):
         s = torch.cuda.Stream(device=dev)
         if all(overlaps(c, s) and overlaps(s, c) for c in chosen):
             chosen.append(s)
             if len(chosen) == n:
                 break
+        else:
+            rest.append(s)
     del long_region, short_region, sink_long, sink_short
-    if len(chosen) < n:
-        raise RuntimeError(f"found only {len(chosen)} of {n} streams that run side by side")
-    return chosen
+    overlap = len(chosen) == n
+    chosen += rest[:n - len(chosen)]
+    return chosen, overlap

@@ -91,6 +91,8 @@ for _name in ("llmig_migration_abort", "llmig_migration_commit"):
     getattr(_lib, _name).restype = ctypes.c_int
 _lib.llmig_migration_set_max_workgroups.argtypes = [_vp, ctypes.c_int32]
 _lib.llmig_migration_set_max_workgroups.restype = ctypes.c_int
+_lib.llmig_migration_set_stage_events.argtypes = [_vp, _vp, _vp]
+_lib.llmig_migration_set_stage_events.restype = ctypes.c_int
 _lib.llmig_migration_info.argtypes = [_vp, ctypes.POINTER(ctypes.c_int32), _i64p, _i64p, _i64p]
 _lib.llmig_migration_info.restype = ctypes.c_int
 _lib.llmig_decode_attention_workspace.argtypes = [_vp, ctypes.c_int32, ctypes.c_int32, ctypes.c_int32,
@@ -287,6 +289,15 @@ class MigrationHandle:
     def set_max_workgroups(self, n: int) -> None:
         """Cap the copy grid (0: uncapped) to leave bandwidth to decoding."""
         _check(_lib.llmig_migration_set_max_workgroups(self._h, int(n)), "llmig_migration_set_max_workgroups")
+
+    def set_stage_events(self, start, stop) -> None:
+        """Time the next stage's kernels with two torch timing events (the
+        events are recorded once here so they exist)."""
+        st = torch.cuda.current_stream()
+        for e in (start, stop):
+            e.record(st)
+        _check(_lib.llmig_migration_set_stage_events(self._h, start.cuda_event, stop.cuda_event),
+               "llmig_migration_set_stage_events")
 
     def info(self):
         st, cp, rs, ns = ctypes.c_int32(), ctypes.c_int64(), ctypes.c_int64(), ctypes.c_int64()

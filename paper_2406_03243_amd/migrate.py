@@ -76,11 +76,13 @@ class Migration:
         block."""
         ev = None
         if time_it:
+            # recorded by the library as the stage's first kernel starts and
+            # its last kernel ends: kernel time, without host launch latency
             ev = (torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
-            ev[0].record(self.stream)
+            self.coord.set_stage_events(*ev)
         n = self.coord.stage(self.src, self.dst, self.src_table, length, final, self.free, stream=self.stream)
-        if time_it:
-            ev[1].record(self.stream)
+        if time_it and n == 0:
+            ev = None
         end = length if final else (length // self.bs) * self.bs
         rec = StageRecord(length, self.copied_tok, end, n, final)
         self.stages.append(rec)

@@ -80,7 +80,7 @@ def test_llama7b_multistage_full():
     guard_before = compact(su.dst, guard)
     host_appends = [a.cpu().numpy().reshape(su.shape.num_layers, 2, c, su.src.slot_bytes)
                     for a, c in zip(su.appends, su.counts)]
-    mig, dec = harness.concurrent_streams(2)
+    mig, dec = harness.concurrent_streams(2)[0]
     m, downtime = migrate.run_scheduled(su.src, su.dst, table, free, su.lengths[0], su.appends, mig, dec)
     torch.cuda.synchronize()
     assert len(m.stages) == 5 and m.stages[-1].final
@@ -112,7 +112,7 @@ def test_llama30b_quarter_full_16k():
     cap = 1040
     hs = compact(su.src, table[:cap])
     hd = compact(su.dst, free[:cap])
-    mig, dec = harness.concurrent_streams(2)
+    mig, dec = harness.concurrent_streams(2)[0]
     pool = su.extra["append_pool"]
     m, downtime = migrate.run_timed(su.src, su.dst, table, length, free, pool, mig, dec, step_ms=20.0)
     torch.cuda.synchronize()
@@ -176,7 +176,7 @@ def test_batched_host_staged_full(mode):
     if mode == "copy_engine":
         dev_bufs = [(torch.empty(nbytes, dtype=torch.uint8, device="cuda"),
                      torch.empty(nbytes, dtype=torch.uint8, device="cuda")) for _ in range(2)]
-    migrate.run_host_staged(su.src, su.dst, ms, md, bufs, *harness.concurrent_streams(2), chunk,
+    migrate.run_host_staged(su.src, su.dst, ms, md, bufs, *harness.concurrent_streams(2)[0], chunk,
                             dev_bufs=dev_bufs)
     torch.cuda.synchronize()
     ids = np.arange(len(sample), dtype=np.int32)
@@ -199,7 +199,7 @@ def test_gqa_long_under_load():
     region = su.extra["region"]
     wgs = torch.cuda.get_device_properties(0).multi_processor_count * 4
     sink = torch.empty(wgs * 256, dtype=torch.int64, device="cuda")
-    rd, mig, dec = harness.concurrent_streams(3)
+    rd, mig, dec = harness.concurrent_streams(3)[0]
     llmig_stream_read(region, 2, wgs, sink, stream=rd)
     m, downtime = migrate.run_timed(su.src, su.dst, table, length, free, pool, mig, dec, step_ms=20.0)
     torch.cuda.synchronize()

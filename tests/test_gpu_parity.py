@@ -82,7 +82,9 @@ STAGE_CASES = [
     (4, 90, 90, 16, 5, 72, 77, False),        # 11.25 KiB: a partial last row
     (2, 50, 50, 1, 1, 8, 50, False),          # 16-byte tiles
     (1, 40, 40, 8, 1, 8, 1, False),           # 128-byte tiles, a single pair
-    (2, 600, 600, 16, 32, 128, 512, False),   # LLaMA-7B tiles (128 KiB)
+    (2, 600, 600, 16, 32, 128, 512, False),   # LLaMA-7B tiles (128 KiB): one launch of 16-bit ids
+    (2, 70000, 66000, 1, 1, 8, 300, False),   # ids past 65535: 32-bit inline ids, two launches
+    (1, 66000, 70000, 1, 1, 8, 520, True),
 ]
 
 
@@ -183,7 +185,7 @@ def test_multistage_scheduled_small():
     free, _ = wl.free_list(seed, shape.num_blocks, 0.3)
     data = _appends(shape, seed, counts, src.slot_bytes)
     hs, hd = host_image(src), host_image(dst)
-    mig, dec = harness.concurrent_streams(2)
+    mig, dec = harness.concurrent_streams(2)[0]
     m, downtime = migrate.run_scheduled(src, dst, table, free, initial,
                                         [torch.from_numpy(x).cuda() for x in data], mig, dec)
     torch.cuda.synchronize()
@@ -225,7 +227,7 @@ def test_multistage_timed_small():
     llmig.llmig_write_tokens(wa, [0], 0, torch.zeros(6 * 2 * src.slot_bytes, dtype=torch.uint8, device="cuda"))
     torch.cuda.synchronize()
     hs, hd = host_image(src), host_image(dst)
-    mig, dec = harness.concurrent_streams(2)
+    mig, dec = harness.concurrent_streams(2)[0]
     # a very short simulated decode step forces several stages
     m, downtime = migrate.run_timed(src, dst, table, initial, free, torch.from_numpy(append_pool).cuda(),
                                     mig, dec, step_ms=0.005, last_stage_max_blocks=1, max_stages=6)
@@ -410,3 +412,37 @@ def test_concurrent_stages_from_threads():
                 orc.copy_layout(hs, (0, 0), want, layouts[j], ms, md, 4, 64, 2)
         assert_same(host_image(d), want, f"destination {j}")
     assert_same(host_image(src), hs, "source")
+
+
+def test_stage_events_bracket_the_kernels():
+    """llmig_migration_set_stage_events: the events come back recorded at the
+    stage's first kernel start and last kernel end, inside events recorded on
+    the stream around the call, and apply to one call only."""
+    say("stage events")
+    shape = wl.PoolShape(2, 1300, 16, 8, 128, "fp16")
+    src = make_pool(shape, 9200, wl.SRC_VALUES)
+    dst = make_pool(shape, 9200, wl.DST_VALUES)
+    table = np.arange(0, 1300, 2, dtype=np.int32)[:601]
+    free = np.arange(1, 1300, 2, dtype=np.int32)
+    h = llmig.MigrationHandle(16)
+    st = torch.cuda.Stream()
+    outer = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+    inner = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+    h.set_stage_events(*inner)
+    torch.cuda.synchronize()
+    outer[0].record(st)
+    n = h.stage(src, dst, table, 600 * 16, False, free, stream=st)   # 600 pairs: two launches
+    outer[1].record(st)
+    torch.cuda.synchronize()
+    assert n == 600
+    t_in = inner[0].elapsed_time(inner[1])
+    t_out = outer[0].elapsed_time(outer[1])
+    assert 0 < t_in <= t_out, (t_in, t_out)
+    assert outer[0].elapsed_time(inner[0]) >= 0 and inner[1].elapsed_time(outer[1]) >= 0
+    # the next call is not timed: the events keep their values
+    before = inner[0].elapsed_time(inner[1])
+    h.stage(src, dst, table, 600 * 16 + 5, True, free[600:], stream=st)
+    torch.cuda.synchronize()
+    assert inner[0].elapsed_time(inner[1]) == before
+    hs = HostPool(harness.snapshot(src.k), harness.snapshot(src.v), 16, src.slot_bytes)
+    assert oracle.default().first_token_mismatch(hs, table, host_image(dst), free[:601], 600 * 16 + 5) == -1

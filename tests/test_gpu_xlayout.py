@@ -162,7 +162,7 @@ def test_multistage_cross_layout(layouts):
                     for k, c in enumerate(counts)]
     appends = [torch.from_numpy(a).cuda() for a in appends_host]
     hs, hd = host_image(src), host_image(dst)
-    mig_stream, dec_stream = harness.concurrent_streams(2)
+    mig_stream, dec_stream = harness.concurrent_streams(2)[0]
     m, _ = migrate.run_scheduled(src, dst, table, free, initial, appends, mig_stream, dec_stream)
     torch.cuda.synchronize()
     dst_table = m.commit()
