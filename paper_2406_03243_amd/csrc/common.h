@@ -16,6 +16,13 @@ constexpr int kThreads = 256;                 // 4 wavefronts of 64 lanes
 constexpr uint32_t kRowBytes = kThreads * 16; // one 16-byte word per lane of a workgroup
 constexpr int kInlinePairs = 256;             // ids carried in the kernel arguments per launch
 
+// Where a launch finds its block ids.
+enum Ids {
+    kIdsDevice = 0, // device arrays src_ids_dev / dst_ids_dev
+    kIds32 = 1,     // ids[i] (source) and ids[kInlinePairs + i] (destination)
+    kIds16 = 2,     // ids[i] = source | destination << 16 (pool to pool, ids below 65536)
+};
+
 typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
 
 thread_local int g_last_hip_error = 0;

@@ -35,8 +35,11 @@
 //  * Index arithmetic divides chunk numbers (< 2^16) by per-call constants
 //    with a multiply-high by ceil(2^32 / divisor), exact in that range.
 //  * Block ids, layouts and base addresses are wavefront-uniform and come
-//    from the kernel arguments or scalar loads; ids of up to kInlinePairs
-//    pairs travel inline, as in the same-layout copy.
+//    from the kernel arguments or scalar loads; ids travel inline as in the
+//    same-layout copy (512 pairs of packed 16-bit ids a launch when both
+//    pools have at most 65536 blocks, else 256 pairs of 32-bit ids).
+//  * Global accesses are raw buffer loads and stores over one tile with the
+//    same cache policy as the same-layout copy (nt loads, sc1 nt stores).
 //  * The source may also be a staging buffer laid out as llmig_pack writes
 //    it (the receiving side of block fusion, §5, converting as it scatters).
 #pragma once
@@ -71,8 +74,7 @@ struct ConvertArgs {
     uint32_t lin_first;         // this launch's first pair within the whole call
     uint32_t lin_pairs;         // pairs in the whole call (plane stride of the staging buffer)
     int32_t layouts[4];         // source K, source V, destination K, destination V
-    int32_t src_ids[kInlinePairs];
-    int32_t dst_ids[kInlinePairs];
+    uint32_t ids[2 * kInlinePairs]; // inline ids, laid out as the launch's Ids mode says
 };
 
 __device__ __forceinline__ uint32_t div_magic(uint32_t n, uint64_t magic)
@@ -110,7 +112,23 @@ __device__ __forceinline__ void wave_lds_sync()
     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
 }
 
-template <bool INLINE_IDS, int N>
+template <int IDS>
+__device__ __forceinline__ uint32_t convert_src_id(const ConvertArgs &a, uint32_t i)
+{
+    if (IDS == kIds16)
+        return a.ids[i] & 0xffffu;
+    return IDS == kIds32 ? a.ids[i] : static_cast<uint32_t>(id_entry(a.src_ids_dev, i));
+}
+
+template <int IDS>
+__device__ __forceinline__ uint32_t convert_dst_id(const ConvertArgs &a, uint32_t i)
+{
+    if (IDS == kIds16)
+        return a.ids[i] >> 16;
+    return IDS == kIds32 ? a.ids[kInlinePairs + i] : static_cast<uint32_t>(id_entry(a.dst_ids_dev, i));
+}
+
+template <int IDS, int N>
 __global__ void __launch_bounds__(kConvertWaves * 64) convert_tiles(const ConvertArgs a)
 {
     __shared__ u32x4 lds[kConvertWaves][68 * N];     // 64 N chunks + one pad per 16
@@ -135,27 +153,27 @@ __global__ void __launch_bounds__(kConvertWaves * 64) convert_tiles(const Conver
         if (a.src_lin) {
             s = a.src_lin + (static_cast<uint64_t>(plane) * a.lin_pairs + a.lin_first + i) * a.tile_bytes;
         } else {
-            const int32_t sid = INLINE_IDS ? a.src_ids[i] : id_entry(a.src_ids_dev, i);
             s = reinterpret_cast<const uint8_t *>(table_entry(a.src_tab, kv * a.num_layers + layer)) +
-                static_cast<uint64_t>(uniform(static_cast<uint32_t>(sid))) * a.tile_bytes;
+                static_cast<uint64_t>(uniform(convert_src_id<IDS>(a, i))) * a.tile_bytes;
         }
-        const int32_t did = INLINE_IDS ? a.dst_ids[i] : id_entry(a.dst_ids_dev, i);
         uint8_t *d = reinterpret_cast<uint8_t *>(table_entry(a.dst_tab, kv * a.num_layers + layer)) +
-                     static_cast<uint64_t>(uniform(static_cast<uint32_t>(did))) * a.tile_bytes;
+                     static_cast<uint64_t>(uniform(convert_dst_id<IDS>(a, i))) * a.tile_bytes;
+        const __amdgpu_buffer_rsrc_t rs = tile_rsrc(s, a.tile_bytes);
+        const __amdgpu_buffer_rsrc_t rd = tile_rsrc(d, a.tile_bytes);
 
         u32x4 r[N];
 #pragma unroll
         for (int u = 0; u < N; ++u) {
             const uint32_t k = lane + 64u * u;
             if (k < a.chunks)
-                r[u] = load16(s + slab_offset(sl, h, k, a));
+                r[u] = buffer_load16(rs, slab_offset(sl, h, k, a));
         }
         if (sl == dl) {
 #pragma unroll
             for (int u = 0; u < N; ++u) {
                 const uint32_t k = lane + 64u * u;
                 if (k < a.chunks)
-                    store16(d + slab_offset(dl, h, k, a), r[u]);
+                    buffer_store16(rd, slab_offset(dl, h, k, a), r[u]);
             }
             continue;
         }
@@ -204,25 +222,32 @@ __global__ void __launch_bounds__(kConvertWaves * 64) convert_tiles(const Conver
                     v = mine[padded(dim_chunk_index(sl, t, c, a))];
                 }
             }
-            store16(d + slab_offset(dl, h, k, a), v);
+            buffer_store16(rd, slab_offset(dl, h, k, a), v);
         }
         wave_lds_sync();
     }
 }
 
-template <bool INLINE_IDS>
+template <int IDS>
 const void *convert_kernel_n(int n)
 {
     switch (n) {
     case 8:
-        return reinterpret_cast<const void *>(&convert_tiles<INLINE_IDS, 8>);
+        return reinterpret_cast<const void *>(&convert_tiles<IDS, 8>);
     case 4:
-        return reinterpret_cast<const void *>(&convert_tiles<INLINE_IDS, 4>);
+        return reinterpret_cast<const void *>(&convert_tiles<IDS, 4>);
     case 2:
-        return reinterpret_cast<const void *>(&convert_tiles<INLINE_IDS, 2>);
+        return reinterpret_cast<const void *>(&convert_tiles<IDS, 2>);
     default:
-        return reinterpret_cast<const void *>(&convert_tiles<INLINE_IDS, 1>);
+        return reinterpret_cast<const void *>(&convert_tiles<IDS, 1>);
     }
+}
+
+const void *convert_kernel(int ids, int n)
+{
+    if (ids == kIdsDevice)
+        return convert_kernel_n<kIdsDevice>(n);
+    return ids == kIds16 ? convert_kernel_n<kIds16>(n) : convert_kernel_n<kIds32>(n);
 }
 
 uint64_t magic_for(uint32_t divisor)
@@ -243,9 +268,13 @@ int convert_chunks_per_lane(uint32_t chunks)
 // buffer a.src_lin, one tile per pair and plane).  The caller has checked
 // that the geometry is supported (16-bit elements, head_dim % 8 == 0,
 // block_size % 8 == 0 when a side is HDN, slabs of at most 8 KiB).
+// ids16: every id of both lists is below 65536 (pool to pool only).
 int launch_convert(ConvertArgs a, const int32_t *src_ids, const int32_t *dst_ids, int64_t n, bool ids_on_device,
-                   hipStream_t stream, uint32_t max_workgroups, const LaunchEvents &ev = LaunchEvents())
+                   hipStream_t stream, uint32_t max_workgroups, const LaunchEvents &ev = LaunchEvents(),
+                   bool ids16 = false)
 {
+    const int ids = ids_on_device ? kIdsDevice : (src_ids && ids16) ? kIds16 : kIds32;
+    const uint64_t inline_pairs = ids == kIds16 ? 2 * kInlinePairs : kInlinePairs;
     const int per_lane = convert_chunks_per_lane(a.chunks);
     if (per_lane > kMaxSlabChunksPerLane)
         return LLMIG_EINVAL;
@@ -254,23 +283,26 @@ int launch_convert(ConvertArgs a, const int32_t *src_ids, const int32_t *dst_ids
     a.magic_t = magic_for(a.t_chunks > 0 ? a.t_chunks : 1u);
     const uint64_t units_per_pair = 2ull * a.num_layers * a.heads;
     const uint64_t per_launch = std::min<uint64_t>(0x7fffffffull / units_per_pair,
-                                                   ids_on_device ? UINT64_MAX : kInlinePairs);
+                                                   ids_on_device ? UINT64_MAX : inline_pairs);
     if (per_launch == 0)
         return LLMIG_EINVAL;
-    const void *fn = ids_on_device ? convert_kernel_n<false>(per_lane) : convert_kernel_n<true>(per_lane);
+    const void *fn = convert_kernel(ids, per_lane);
     a.lin_pairs = static_cast<uint32_t>(n);
     const int64_t launches = (n + static_cast<int64_t>(per_launch) - 1) / static_cast<int64_t>(per_launch);
     for (int64_t first = 0, k = 0; first < n; first += static_cast<int64_t>(per_launch), ++k) {
         const uint32_t m = static_cast<uint32_t>(std::min<int64_t>(n - first, per_launch));
         a.units = static_cast<uint32_t>(m * units_per_pair);
         a.lin_first = static_cast<uint32_t>(first);
-        if (ids_on_device) {
+        if (ids == kIdsDevice) {
             a.src_ids_dev = src_ids ? src_ids + first : nullptr;
             a.dst_ids_dev = dst_ids + first;
+        } else if (ids == kIds16) {
+            for (uint32_t k = 0; k < m; ++k)
+                a.ids[k] = static_cast<uint32_t>(src_ids[first + k]) | (static_cast<uint32_t>(dst_ids[first + k]) << 16);
         } else {
             if (src_ids)
-                std::memcpy(a.src_ids, src_ids + first, m * sizeof(int32_t));
-            std::memcpy(a.dst_ids, dst_ids + first, m * sizeof(int32_t));
+                std::memcpy(a.ids, src_ids + first, m * sizeof(int32_t));
+            std::memcpy(a.ids + kInlinePairs, dst_ids + first, m * sizeof(int32_t));
         }
         void *args[] = {&a};
         uint32_t grid = (a.units + kConvertWaves - 1) / kConvertWaves;

@@ -50,12 +50,6 @@ namespace {
 
 enum Side { kPool = 0, kLinear = 1 };
 
-// Where a launch finds its block ids.
-enum Ids {
-    kIdsDevice = 0, // device arrays src_ids_dev / dst_ids_dev
-    kIds32 = 1,     // ids[i] (source) and ids[kInlinePairs + i] (destination)
-    kIds16 = 2,     // ids[i] = source | destination << 16 (pool to pool)
-};
 
 // Arguments of one copy launch.  Pool sides address tile (l, kv, id) at
 // tab[kv * L + l] + id * tile_bytes; linear sides address pair i of plane

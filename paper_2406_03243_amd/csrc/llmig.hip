@@ -302,7 +302,8 @@ int launch_stage(const llmig_pool *src, const llmig_pool *dst, const int32_t *ms
         ConvertArgs c = convert_args(src, src->layouts, dst->layouts);
         c.src_tab = src->d_tab;
         c.dst_tab = dst->d_tab;
-        return launch_convert(c, ms, md, n, ids_on_device, stream, max_workgroups, ev);
+        const bool ids16 = src->num_blocks <= 65536 && dst->num_blocks <= 65536;
+        return launch_convert(c, ms, md, n, ids_on_device, stream, max_workgroups, ev, ids16);
     }
     CopyArgs a;
     std::memset(&a, 0, sizeof(a));

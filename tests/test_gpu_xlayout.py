@@ -293,3 +293,11 @@ def test_unpack_layout_errors_and_plain_case():
     t = pool.tile_bytes
     assert np.array_equal(got.k[0][0], data[:t]) and np.array_equal(got.k[0][1], data[t:2 * t])
     assert np.array_equal(got.v[0][0], data[2 * t:3 * t]) and np.array_equal(got.v[0][1], data[3 * t:])
+
+
+def test_convert_pools_past_16_bit_ids():
+    # 70000-block pools: ids past 65535 travel as 32-bit words, 256 pairs a launch
+    shape = wl.PoolShape(2, 70000, 8, 2, 8, "fp16")
+    sl, dl = (NHD, HCNX), (HDN, NHD)
+    say("convert, 70000-block pools", lay_name(sl, dl))
+    run_stage(shape, sl, dl, 300, seed=9300, nbd=66000)
