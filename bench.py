@@ -390,8 +390,10 @@ def downtime_sweep(reps):
 
 
 def batched_section(reps=20, host_reps=3, chunk_pairs=64):
-    """64 requests migrated in one llmig_stage call; and the same pairs
-    through pinned host memory (pack -> host -> unpack, chunked, two buffers)."""
+    """64 requests migrated in one llmig_stage call; the same pairs packed
+    into and unpacked from device staging (block fusion's kernels alone);
+    and the same pairs through pinned host memory (pack -> host -> unpack,
+    chunked, two buffers)."""
     import torch
 
     from paper_2406_03243_amd import harness, migrate, scenarios
@@ -421,6 +423,31 @@ def batched_section(reps=20, host_reps=3, chunk_pairs=64):
            "GBps": round(nbytes / (us * 1e-6) / 1e9, 1),
            "lengths": {"min": int(min(su.lengths)), "median": float(statistics.median(su.lengths)),
                        "max": int(max(su.lengths)), "tokens": int(sum(su.lengths))}}
+    # block fusion with device staging: the pack and unpack kernels alone,
+    # each reading and writing every tile once (HBM-bound)
+    from paper_2406_03243_amd.llmig import llmig_pack, llmig_unpack
+    one_way_all = len(ms) * shape.num_layers * 2 * src.tile_bytes
+    staging = torch.empty(one_way_all, dtype=torch.uint8, device="cuda")
+    for name, fn, ids in (("pack", llmig_pack, ms), ("unpack", llmig_unpack, md)):
+        pool = src if name == "pack" else dst
+        for _ in range(3):
+            fn(pool, ids, staging, stream=mig)
+        torch.cuda.synchronize()
+        t = []
+        for _ in range(reps):
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record(mig)
+            fn(pool, ids, staging, stream=mig)
+            e1.record(mig)
+            torch.cuda.synchronize()
+            t.append(e0.elapsed_time(e1) * 1e3)
+        gbs = 2 * one_way_all / (statistics.median(t) * 1e-6) / 1e9
+        out[f"{name}_device_staging"] = {"bytes": 2 * one_way_all, "us": spread(t), "GBps": round(gbs, 1),
+                                         "hbm_frac": round(gbs / HBM_PEAK_GBS, 3)}
+        log("batched", name, out[f"{name}_device_staging"])
+    del staging
+    torch.cuda.synchronize()
+    torch.cuda.empty_cache()
     chunk_bytes = chunk_pairs * shape.num_layers * 2 * src.tile_bytes
     bufs = [torch.empty(chunk_bytes, dtype=torch.uint8, pin_memory=True) for _ in range(2)]
     dev_bufs = [(torch.empty(chunk_bytes, dtype=torch.uint8, device="cuda"),
