@@ -448,8 +448,10 @@ int llmig_plan(const int32_t *src_table, int64_t src_table_len, const int32_t *d
             return LLMIG_ERANGE;
     if (has_repeat_any(src, n) || has_repeat_any(dst_free_list, n))
         return LLMIG_EINVAL;
-    std::memcpy(out_src, src, static_cast<size_t>(n) * sizeof(int32_t));
-    std::memcpy(out_dst, dst_free_list, static_cast<size_t>(n) * sizeof(int32_t));
+    if (n > 0) { // the output arrays may be NULL for an empty stage
+        std::memcpy(out_src, src, static_cast<size_t>(n) * sizeof(int32_t));
+        std::memcpy(out_dst, dst_free_list, static_cast<size_t>(n) * sizeof(int32_t));
+    }
     *out_n = n;
     return LLMIG_OK;
 }
