@@ -283,10 +283,11 @@ int llmig_migration_stage(llmig_migration *m, const llmig_pool *src, const llmig
 int llmig_migration_set_max_workgroups(llmig_migration *m, int32_t max_workgroups);
 
 /* Times the next llmig_migration_stage call on the GPU: start_event (a
- * hipEvent_t, NULL for none) is recorded as the stage's first kernel starts
- * and stop_event as its last kernel ends, so their interval is the stage's
- * kernel time without the host's launch latency (events recorded on the
- * stream around the call include it).  The events are the caller's,
+ * hipEvent_t, NULL for none) is recorded on the stage's stream right before
+ * its first kernel is launched and stop_event right after its last, so
+ * their interval is the stage's kernel time plus one launch latency, without
+ * the host work that plans and checks the stage (events recorded on the
+ * stream around the call include that).  The events are the caller's,
  * created with timing enabled; they apply to that one call, which records
  * nothing if its stage is empty or fails before launching.  Host only;
  * LLMIG_EINVAL for m == NULL. */

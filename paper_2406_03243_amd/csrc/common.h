@@ -3,7 +3,6 @@
 // Part of the single translation unit built from llmig.hip.
 #pragma once
 
-#include <hip/hip_ext.h>
 #include <hip/hip_runtime.h>
 
 #include <cstdint>
@@ -33,9 +32,10 @@ int hip_error(hipError_t e)
     return LLMIG_EHIP;
 }
 
-// Optional events around a call's kernels: start is recorded when the first
-// kernel starts and stop when the last one ends (no host launch latency in
-// between, unlike events recorded on the stream around the call).
+// Optional events around a call's kernels: start is recorded on the stream
+// right before the first kernel is launched and stop right after the last
+// one, so their interval holds the kernels (and one launch's latency) but
+// none of the host work that planned them.
 struct LaunchEvents {
     hipEvent_t start = nullptr;
     hipEvent_t stop = nullptr;
@@ -45,11 +45,14 @@ struct LaunchEvents {
 hipError_t launch_kernel(const void *fn, dim3 grid, dim3 block, void **args, hipStream_t stream,
                          const LaunchEvents &ev, int64_t k, int64_t launches)
 {
-    hipEvent_t start = k == 0 ? ev.start : nullptr;
-    hipEvent_t stop = k == launches - 1 ? ev.stop : nullptr;
-    if (!start && !stop)
-        return hipLaunchKernel(fn, grid, block, args, 0, stream);
-    return hipExtLaunchKernel(fn, grid, block, args, 0, stream, start, stop, 0);
+    hipError_t e = hipSuccess;
+    if (k == 0 && ev.start)
+        e = hipEventRecord(ev.start, stream);
+    if (e == hipSuccess)
+        e = hipLaunchKernel(fn, grid, block, args, 0, stream);
+    if (e == hipSuccess && k == launches - 1 && ev.stop)
+        e = hipEventRecord(ev.stop, stream);
+    return e;
 }
 
 // Address spaces: global for the copied bytes (global_load/global_store

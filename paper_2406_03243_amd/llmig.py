@@ -173,7 +173,8 @@ class Pool:
         return self._handle
 
     def close(self) -> None:
-        if getattr(self, "_handle", None) is not None:
+        # at interpreter exit the module's globals may already be gone
+        if getattr(self, "_handle", None) is not None and _lib is not None:
             _lib.llmig_pool_destroy(self._handle)
             self._handle = None
 
@@ -279,7 +280,7 @@ class MigrationHandle:
         self.block_size = int(block_size)
 
     def close(self):
-        if getattr(self, "_h", None) is not None:
+        if getattr(self, "_h", None) is not None and _lib is not None:
             _lib.llmig_migration_destroy(self._h)
             self._h = None
 
@@ -291,8 +292,9 @@ class MigrationHandle:
         _check(_lib.llmig_migration_set_max_workgroups(self._h, int(n)), "llmig_migration_set_max_workgroups")
 
     def set_stage_events(self, start, stop) -> None:
-        """Time the next stage's kernels with two torch timing events (the
-        events are recorded once here so they exist)."""
+        """Time the next stage's kernels with two torch timing events, which
+        the library records right before its first launch and right after its
+        last (they are recorded once here so that they exist)."""
         st = torch.cuda.current_stream()
         for e in (start, stop):
             e.record(st)

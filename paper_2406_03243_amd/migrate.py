@@ -76,8 +76,8 @@ class Migration:
         block."""
         ev = None
         if time_it:
-            # recorded by the library as the stage's first kernel starts and
-            # its last kernel ends: kernel time, without host launch latency
+            # recorded by the library right around its launches: kernel time
+            # without the host work that plans and checks the stage
             ev = (torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
             self.coord.set_stage_events(*ev)
         n = self.coord.stage(self.src, self.dst, self.src_table, length, final, self.free, stream=self.stream)
