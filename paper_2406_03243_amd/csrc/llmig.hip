@@ -172,8 +172,9 @@ int check_ids(const int32_t *ids, int64_t n, int32_t num_blocks)
     return LLMIG_OK;
 }
 
-// Whether ids[0..n) holds a repeat; ids are known to lie in [0, num_blocks).
-bool has_repeat(const int32_t *ids, int64_t n, int32_t num_blocks)
+// Whether ids[0..n) holds a repeat; ids are known to lie in [0, bound)
+// (bound may be 0 when n <= 32).  Pairwise for short lists, else a bitmap.
+bool has_repeat(const int32_t *ids, int64_t n, int64_t bound)
 {
     if (n <= 32) {
         for (int64_t a = 0; a < n; ++a)
@@ -182,20 +183,28 @@ bool has_repeat(const int32_t *ids, int64_t n, int32_t num_blocks)
                     return true;
         return false;
     }
-    std::vector<uint8_t> seen(static_cast<size_t>(num_blocks), 0);
+    std::vector<uint64_t> seen(static_cast<size_t>((bound + 63) / 64), 0);
     for (int64_t k = 0; k < n; ++k) {
-        if (seen[ids[k]])
+        const uint64_t bit = 1ull << (ids[k] & 63);
+        uint64_t &word = seen[static_cast<size_t>(ids[k]) >> 6];
+        if (word & bit)
             return true;
-        seen[ids[k]] = 1;
+        word |= bit;
     }
     return false;
 }
 
-// Whether ids[0..n) holds a repeat, for ids of any size (sorts a copy).
+// Whether ids[0..n) holds a repeat, for non-negative ids of any size: a
+// bitmap up to the largest id when that stays small (2 MiB), else a sort.
 bool has_repeat_any(const int32_t *ids, int64_t n)
 {
     if (n <= 32)
         return has_repeat(ids, n, 0);
+    int32_t hi = 0;
+    for (int64_t k = 0; k < n; ++k)
+        hi = std::max(hi, ids[k]);
+    if (hi < (1 << 24))
+        return has_repeat(ids, n, static_cast<int64_t>(hi) + 1);
     std::vector<int32_t> v(ids, ids + n);
     std::sort(v.begin(), v.end());
     return std::adjacent_find(v.begin(), v.end()) != v.end();

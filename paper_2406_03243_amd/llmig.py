@@ -322,11 +322,12 @@ class MigrationHandle:
     def stage(self, src: "Pool", dst: "Pool", src_table: np.ndarray, length: int, final: bool,
               dst_free_list: np.ndarray, stream=None) -> int:
         """Plan, reserve and launch the next stage; returns the number of
-        free-list entries consumed.  The tables must be contiguous int32."""
+        free-list entries consumed."""
+        st, fl = _host_i32(src_table), _host_i32(dst_free_list)
         n = ctypes.c_int64(0)
-        _check(_lib.llmig_migration_stage(self._h, src.handle, dst.handle, src_table.ctypes.data, src_table.size,
-                                          int(length), int(bool(final)), dst_free_list.ctypes.data,
-                                          dst_free_list.size, _stream(stream), ctypes.byref(n)),
+        _check(_lib.llmig_migration_stage(self._h, src.handle, dst.handle, st.ctypes.data, st.size,
+                                          int(length), int(bool(final)), fl.ctypes.data,
+                                          fl.size, _stream(stream), ctypes.byref(n)),
                "llmig_migration_stage")
         return n.value
 
