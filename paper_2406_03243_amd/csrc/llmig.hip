@@ -4,11 +4,12 @@
 // live migration of Llumnix (arXiv 2406.03243) §4.2 with the block fusion
 // of §5; the interface comments in llmig.h state what every call computes.
 //
-// Sources: common.h (shared kernel definitions), copy_tiles.h (the tile
-// copy and its launch configuration), decode_attention.h (paged decode
-// attention, the work measured beside a migration), this file (pool
-// registry, planner, coordinator, harness kernels, argument checks and the
-// C ABI).
+// Sources: common.h (shared kernel definitions, buffer accesses, launch
+// helper), copy_tiles.h (the tile copy and its launch configuration),
+// convert_tiles.h (the copy between pools of different intra-tile
+// layouts), decode_attention.h (paged decode attention, the work measured
+// beside a migration), this file (pool registry, planner, coordinator,
+// harness kernels, argument checks and the C ABI).
 
 #include <hip/hip_runtime.h>
 
