@@ -90,7 +90,11 @@ __global__ void __launch_bounds__(kThreads) attn_reduce(const AttnReduceArgs a)
 //                     and the 16-bit rounding of the remainder, two MFMAs, so
 //                     the weights keep ~2^-16 (bf16) / 2^-22 (fp16) precision.
 // The four wavefronts take alternate token groups of the partition and merge
-// their states through LDS at the end.
+// their states through LDS at the end.  The kernel waits on HBM, not on the
+// matrix cores or LDS, so it is built for four wavefronts per SIMD (at most
+// 128 registers: the accumulators move from AGPRs to VGPRs), which the
+// workgroup's 35 KiB of LDS also allows; measured in one process against
+// the three-wavefront build: 3-6% faster, identical output.
 typedef _Float16 f16x8_t __attribute__((ext_vector_type(8)));
 typedef _Float16 f16x4_t __attribute__((ext_vector_type(4)));
 typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
@@ -132,7 +136,8 @@ __device__ __forceinline__ uint32_t to16(float x)
 }
 
 template <int BF16, int D>
-__global__ void __launch_bounds__(kThreads) attn_partial_mfma(const AttnArgs a)
+__global__ void __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(4, 8)))
+attn_partial_mfma(const AttnArgs a)
 {
     constexpr int KS = D / 32;            // k-steps of the QK product
     constexpr int MT = D / 16;            // 16-dim tiles of the PV product
