@@ -446,3 +446,28 @@ def test_stage_events_bracket_the_kernels():
     assert inner[0].elapsed_time(inner[1]) == before
     hs = HostPool(harness.snapshot(src.k), harness.snapshot(src.v), 16, src.slot_bytes)
     assert oracle.default().first_token_mismatch(hs, table, host_image(dst), free[:601], 600 * 16 + 5) == -1
+
+
+def test_largest_tiles():
+    """Tiles of 2^31 - 16 bytes, the largest a pool accepts: offsets inside a
+    tile and the buffer ranges are at their limits.  Checked on the device:
+    the mapped tiles equal their sources, the others are untouched."""
+    say("largest tiles: 2^31 - 16 bytes")
+    dim = (2 ** 31 - 16) // 2
+    shape = wl.PoolShape(1, 3, 1, 1, dim, "fp16")
+    sk, sv = harness.alloc_layers(shape)
+    dk, dv = harness.alloc_layers(shape)
+    harness.fill_on_device(sk + sv, 9400)
+    harness.fill_on_device(dk + dv, 9401)
+    src, dst = Pool(sk, sv), Pool(dk, dv)
+    assert src.tile_bytes == 2 ** 31 - 16
+    keep = [t[1].clone() for t in dk + dv]
+    llmig.llmig_stage(src, dst, [2], [0])
+    torch.cuda.synchronize()
+    for s_t, d_t, k in zip(sk + sv, dk + dv, keep):
+        assert torch.equal(d_t[0], s_t[2])
+        assert torch.equal(d_t[1], k)
+    del keep
+    k2, v2 = harness.alloc_layers(wl.PoolShape(1, 1, 1, 1, dim + 8, "fp16"))
+    with pytest.raises(LlmigError):                    # 2^31 bytes: one byte past the limit
+        Pool(k2, v2)
