@@ -61,17 +61,35 @@ __global__ void __launch_bounds__(kThreads) attn_reduce(const AttnReduceArgs a)
         const uint32_t b = r % a.batch;
         const uint32_t layer = static_cast<uint32_t>(r / a.batch);
         float m = -INFINITY, l = 0.f, acc = 0.f;
-        for (int32_t p = 0; p < a.seq_count[b]; ++p) {
-            const float *src = a.ws + ((static_cast<uint64_t>(layer) * a.n_items_total + a.seq_first[b] + p) *
-                                           a.q_heads + h) * (a.head_dim + 2);
-            const float m2 = src[0], l2 = src[1], a2 = src[2 + d];
-            const float mm = fmaxf(m, m2);
-            if (mm == -INFINITY)
-                continue;
-            const float c1 = __expf(m - mm), c2 = __expf(m2 - mm);
-            l = l * c1 + l2 * c2;
-            acc = acc * c1 + a2 * c2;
-            m = mm;
+        const int32_t count = a.seq_count[b];
+        const uint64_t stride = static_cast<uint64_t>(a.q_heads) * (a.head_dim + 2); // one partition
+        const float *base = a.ws + ((static_cast<uint64_t>(layer) * a.n_items_total + a.seq_first[b]) * a.q_heads + h) *
+                                       (a.head_dim + 2);
+        // partitions in batches of 8 so their loads are in flight together
+        for (int32_t p0 = 0; p0 < count; p0 += 8) {
+            float m2[8], l2[8], a2[8];
+#pragma unroll
+            for (int u = 0; u < 8; ++u) {
+                m2[u] = -INFINITY;
+                l2[u] = 0.f;
+                a2[u] = 0.f;
+                if (p0 + u < count) {
+                    const float *src = base + (p0 + u) * stride;
+                    m2[u] = src[0];
+                    l2[u] = src[1];
+                    a2[u] = src[2 + d];
+                }
+            }
+#pragma unroll
+            for (int u = 0; u < 8; ++u) {
+                const float mm = fmaxf(m, m2[u]);
+                if (mm == -INFINITY)
+                    continue;
+                const float c1 = __expf(m - mm), c2 = __expf(m2[u] - mm);
+                l = l * c1 + l2[u] * c2;
+                acc = acc * c1 + a2[u] * c2;
+                m = mm;
+            }
         }
         a.out[x] = l > 0.f ? acc / l : 0.f;
     }
