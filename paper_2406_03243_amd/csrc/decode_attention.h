@@ -20,7 +20,7 @@
 
 namespace {
 
-constexpr int kPartTokens = 512;     // tokens per partition
+constexpr int kPartTokens = 1024;    // tokens per partition
 constexpr int kAttnItems = 128;      // (sequence, partition) items per launch, in the kernel arguments
 constexpr int kAttnMaxBatch = 256;   // sequences per call (per-sequence item ranges ride in the arguments)
 
