@@ -71,7 +71,7 @@ CASES = [
     (2, 200, 16, 4, 64, 1, [513, 31, 7], "bf16"),
     (1, 400, 16, 2, 128, 4, [4096, 5, 2000], "bf16"),
     (3, 100, 8, 1, 64, 2, [96, 95, 97, 1], "fp16"),
-    (1, 2000, 16, 1, 128, 2, [30000, 29999, 20000], "fp16"),  # 158 partitions: two launches of items
+    (1, 3200, 16, 1, 128, 2, [50000, 49999, 40000], "fp16"),  # 138 partitions of 1024: two launches of items
     (2, 120, 16, 1, 128, 16, [700, 33], "bf16"),               # 16 query heads on one KV head
     (1, 300, 4, 2, 64, 4, [1000, 3, 62], "bf16"),             # 4-token blocks: a 16-token group spans blocks
 ]
