@@ -163,7 +163,7 @@ int llmig_plan(const int32_t *src_table, int64_t src_table_len,
  * When the pools' K or V layouts differ, every element of each tile moves
  * to its place in the destination's layout (see LLMIG_LAYOUT_*).  That
  * needs elem_bytes == 2, head_dim % 8 == 0, block_size % 8 == 0 if either
- * side uses HDN, and block_size * head_dim * 2 <= 8192 (one head's slab of
+ * side uses HDN, and block_size * head_dim * 2 <= 16384 (one head's slab of
  * a tile); else LLMIG_EINVAL. */
 int llmig_stage(const llmig_pool *src, const llmig_pool *dst,
                 const int32_t *map_src, const int32_t *map_dst, int64_t n,
@@ -196,7 +196,7 @@ int llmig_unpack(const llmig_pool *dst, const int32_t *blocks, int64_t n, int ma
  * untouched with its two layout codes.  Staging layouts equal to dst's make
  * it llmig_unpack.  Converting needs the conditions of a cross-layout
  * llmig_stage (elem_bytes == 2, head_dim % 8 == 0, block_size % 8 == 0 when
- * a side is HDN, block_size * head_dim * 2 <= 8192); else LLMIG_EINVAL, as
+ * a side is HDN, block_size * head_dim * 2 <= 16384); else LLMIG_EINVAL, as
  * for an unknown layout code.  Other arguments and errors as llmig_unpack. */
 int llmig_unpack_layout(const llmig_pool *dst, const int32_t *blocks, int64_t n, int map_on_device,
                         const void *staging, int64_t staging_bytes, int32_t staging_k_layout,

@@ -51,7 +51,7 @@
 
 namespace {
 
-constexpr int kMaxSlabChunksPerLane = 8;            // slabs of up to 8 KiB
+constexpr int kMaxSlabChunksPerLane = 16;           // slabs of up to 16 KiB
 constexpr int kConvertWaves = 2;                    // wavefronts per workgroup
 
 struct ConvertArgs {
@@ -184,7 +184,10 @@ __global__ void __launch_bounds__(kConvertWaves * 64) convert_tiles(const Conver
                 mine[padded(k)] = r[u];
         }
         wave_lds_sync();
-#pragma unroll
+        // Output chunks: fully unrolled for small slabs; for large ones two at
+        // a time, which keeps the gathers' registers within four waves' share.
+        constexpr int kGatherUnroll = N > 4 ? 2 : N;
+#pragma unroll kGatherUnroll
         for (int u = 0; u < N; ++u) {
             const uint32_t k = lane + 64u * u;
             if (k >= a.chunks)
@@ -232,6 +235,8 @@ template <int IDS>
 const void *convert_kernel_n(int n)
 {
     switch (n) {
+    case 16:
+        return reinterpret_cast<const void *>(&convert_tiles<IDS, 16>);
     case 8:
         return reinterpret_cast<const void *>(&convert_tiles<IDS, 8>);
     case 4:
@@ -267,7 +272,7 @@ int convert_chunks_per_lane(uint32_t chunks)
 // Launches the conversion of n pairs (src_ids null: the source is the staging
 // buffer a.src_lin, one tile per pair and plane).  The caller has checked
 // that the geometry is supported (16-bit elements, head_dim % 8 == 0,
-// block_size % 8 == 0 when a side is HDN, slabs of at most 8 KiB).
+// block_size % 8 == 0 when a side is HDN, slabs of at most 16 KiB).
 // ids16: every id of both lists is below 65536 (pool to pool only).
 int launch_convert(ConvertArgs a, const int32_t *src_ids, const int32_t *dst_ids, int64_t n, bool ids_on_device,
                    hipStream_t stream, uint32_t max_workgroups, const LaunchEvents &ev = LaunchEvents(),

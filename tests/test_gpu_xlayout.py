@@ -85,6 +85,7 @@ GEOMETRIES = [
     (2, 60, 8, 3, 64, "bf16", 31),      # 1 KiB slabs: one chunk per lane
     (1, 50, 16, 2, 64, "fp16", 17),     # 2 KiB
     (1, 30, 32, 2, 128, "bf16", 9),     # 8 KiB: eight chunks per lane
+    (1, 20, 32, 2, 256, "fp16", 7),     # 16 KiB: sixteen chunks per lane (block 32, head_dim 256)
     (2, 40, 16, 3, 40, "fp16", 13),     # 80 chunks: a partial second round
     (1, 40, 24, 2, 64, "bf16", 11),     # three 8-token groups per dim
 ]
@@ -214,8 +215,8 @@ def test_unsupported_conversions_are_rejected():
     a, b = pools(wl.PoolShape(1, 4, 12, 1, 64, "fp16"), (NHD, NHD), (NHD, HDN))
     with pytest.raises(LlmigError):
         llmig.llmig_stage(a, b, ids, ids)
-    # slabs over 8 KiB
-    a, b = pools(wl.PoolShape(1, 4, 32, 1, 256, "fp16"), (NHD, NHD), (HND, NHD))
+    # slabs over 16 KiB
+    a, b = pools(wl.PoolShape(1, 4, 64, 1, 256, "fp16"), (NHD, NHD), (HND, NHD))
     with pytest.raises(LlmigError):
         llmig.llmig_stage(a, b, ids, ids)
     # 1-byte elements convert nowhere (same layouts still copy)
