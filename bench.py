@@ -64,12 +64,16 @@ def recorded_traffic(kernel: str):
 
 
 def bulk_span_rows(tile_bytes: int) -> int:
-    """The copy kernel's span (1 KiB rows per wavefront) for a bulk launch:
-    the power of two at or above a quarter of the tile, within [2, 32]
-    (mirrors the library's launch configuration, for labelling only)."""
-    quarter = -(-tile_bytes // 4096)
+    """The copy kernel instance (SPAN, in 1 KiB rows per wavefront) of a bulk
+    launch: a tile is cut into four equal spans (more when a span would pass
+    32 rows) and the instance is the power of two at or above the span,
+    within [2, 32] (mirrors the library's launch configuration, for
+    labelling only)."""
+    rows = -(-tile_bytes // 1024)
+    spans = max(min(4, rows), -(-rows // 32))
+    span_rows = -(-rows // spans)
     span = 2
-    while span < 32 and span < quarter:
+    while span < 32 and span < span_rows:
         span *= 2
     return span
 
