@@ -294,10 +294,11 @@ class MigrationHandle:
     def set_stage_events(self, start, stop) -> None:
         """Time the next stage's kernels with two torch timing events, which
         the library records right before its first launch and right after its
-        last (they are recorded once here so that they exist)."""
-        st = torch.cuda.current_stream()
+        last.  An event that torch has not created yet is recorded once here
+        so that it exists; a reused one is passed as it is."""
         for e in (start, stop):
-            e.record(st)
+            if not e.cuda_event:
+                e.record(torch.cuda.current_stream())
         _check(_lib.llmig_migration_set_stage_events(self._h, start.cuda_event, stop.cuda_event),
                "llmig_migration_set_stage_events")
 

@@ -26,6 +26,18 @@ import torch
 from .llmig import MigrationHandle, Pool, llmig_pack, llmig_plan, llmig_unpack, llmig_write_tokens
 
 
+# Timing event pairs whose times have been read, kept for the next stages:
+# creating and first recording a pair costs more host time than the stage's
+# launch itself.
+_spare_timers: list = []
+
+
+def _timer_pair():
+    if _spare_timers:
+        return _spare_timers.pop()
+    return torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+
+
 @dataclass
 class StageRecord:
     length: int        # tokens resident when the stage was planned
@@ -78,10 +90,11 @@ class Migration:
         if time_it:
             # recorded by the library right around its launches: kernel time
             # without the host work that plans and checks the stage
-            ev = (torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+            ev = _timer_pair()
             self.coord.set_stage_events(*ev)
         n = self.coord.stage(self.src, self.dst, self.src_table, length, final, self.free, stream=self.stream)
         if time_it and n == 0:
+            _spare_timers.append(ev)    # not recorded by the library: free again
             ev = None
         end = length if final else (length // self.bs) * self.bs
         rec = StageRecord(length, self.copied_tok, end, n, final)
@@ -100,10 +113,13 @@ class Migration:
         return self.coord.commit()
 
     def collect_times(self) -> None:
-        """Fill in each timed stage's GPU time (after the stream is synchronised)."""
-        for rec, ev in zip(self.stages, self._events):
+        """Fill in each timed stage's GPU time (after the stream is
+        synchronised); the events go back to the spares."""
+        for k, (rec, ev) in enumerate(zip(self.stages, self._events)):
             if ev is not None:
                 rec.gpu_us = ev[0].elapsed_time(ev[1]) * 1e3
+                _spare_timers.append(ev)
+                self._events[k] = None
 
 
 def run_scheduled(src: Pool, dst: Pool, src_table, dst_free_list, initial_len: int, appends,
