@@ -49,7 +49,9 @@ extern "C" {
 #endif
 
 #define LLMIG_OK 0
-#define LLMIG_EINVAL (-1) /* bad argument, range, alignment, shape or duplicate id */
+#define LLMIG_EINVAL (-1) /* bad argument, range, alignment, shape or duplicate id; also
+                             host memory for a call's bookkeeping ran out (no C++
+                             exception ever leaves the library) */
 #define LLMIG_ENOSPC (-2) /* the destination free list cannot hold the stage (§4.2: the
                              pre-allocation fails and the migration aborts) */
 #define LLMIG_ERANGE (-3) /* a block id outside [0, num_blocks) */

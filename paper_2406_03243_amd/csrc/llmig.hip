@@ -16,6 +16,7 @@
 #include <algorithm>
 #include <cstdint>
 #include <cstring>
+#include <memory>
 #include <new>
 #include <utility>
 #include <vector>
@@ -139,6 +140,20 @@ __global__ void __launch_bounds__(kThreads) stream_read_words(const uint8_t *reg
     ((LLMIG_GLOBAL uint64_t *)out)[lane] = folded;
 }
 
+// Runs an entry point's body.  The host code's only exceptions are failed
+// allocations (the id bitmaps, plan scratch, pool bookkeeping); they become
+// LLMIG_EINVAL here instead of crossing the C ABI.  Bodies allocate before
+// they enqueue anything, so such a failure has no effect.
+template <typename Body>
+int no_throw(Body &&body)
+{
+    try {
+        return body();
+    } catch (...) {
+        return LLMIG_EINVAL;
+    }
+}
+
 bool same_geometry(const llmig_pool *a, const llmig_pool *b)
 {
     return a->num_layers == b->num_layers && a->block_size == b->block_size &&
@@ -242,8 +257,9 @@ int fused_copy_checks(const llmig_pool *pool, const int32_t *blocks, int64_t n, 
         return LLMIG_OK;
     if (!blocks || !staging || (reinterpret_cast<uintptr_t>(staging) & 15u))
         return LLMIG_EINVAL;
-    const int64_t need = n * pool->num_layers * 2 * pool->tile_bytes;
-    if (n > (INT64_MAX / 2) / pool->num_layers / pool->tile_bytes || staging_bytes < need)
+    if (n > (INT64_MAX / 2) / pool->num_layers / pool->tile_bytes)
+        return LLMIG_EINVAL;
+    if (staging_bytes < n * pool->num_layers * 2 * pool->tile_bytes)
         return LLMIG_EINVAL;
     if (!map_on_device) {
         int rc = check_ids(blocks, n, pool->num_blocks);
@@ -336,13 +352,20 @@ int next_range(const llmig_migration *m, int64_t len, int final_stage, int64_t *
     return LLMIG_OK;
 }
 
-void record_stage(llmig_migration *m, const int32_t *dst_ids, int64_t n, int64_t to, int final_stage)
+// Adds a planned stage to m.  LLMIG_EINVAL, with m unchanged, when the
+// reservation cannot grow (no exception leaves the library).
+int record_stage(llmig_migration *m, const int32_t *dst_ids, int64_t n, int64_t to, int final_stage)
 {
-    m->reserved.insert(m->reserved.end(), dst_ids, dst_ids + n); // n <= free list: memory the caller holds
+    try {
+        m->reserved.insert(m->reserved.end(), dst_ids, dst_ids + n); // n <= free list: memory the caller holds
+    } catch (...) {
+        return LLMIG_EINVAL;
+    }
     m->copied_tok = to;
     m->stages += 1;
     if (final_stage)
         m->state = LLMIG_MIGRATION_FINISHED;
+    return LLMIG_OK;
 }
 
 } // namespace
@@ -369,51 +392,48 @@ int llmig_pool_create(const llmig_pool_desc *desc, llmig_pool **out)
             (16 % desc->elem_bytes != 0 || (static_cast<int64_t>(desc->head_dim) * desc->elem_bytes) % 16 != 0))
             return LLMIG_EINVAL;
     }
-    const int32_t L = desc->num_layers;
-    std::vector<uint64_t> tab(2 * static_cast<size_t>(L));
-    for (int32_t l = 0; l < L; ++l) {
-        tab[l] = desc->k_ptrs[l];
-        tab[L + l] = desc->v_ptrs[l];
-    }
-    for (uint64_t p : tab)
-        if (p == 0 || (p & 15u))
-            return LLMIG_EINVAL;
-
-    llmig_pool *pool = new (std::nothrow) llmig_pool();
-    if (!pool)
-        return LLMIG_EINVAL;
-    pool->num_layers = L;
-    pool->num_blocks = desc->num_blocks;
-    pool->block_size = desc->block_size;
-    pool->num_kv_heads = desc->num_kv_heads;
-    pool->head_dim = desc->head_dim;
-    pool->elem_bytes = desc->elem_bytes;
-    pool->layouts[0] = desc->k_layout;
-    pool->layouts[1] = desc->v_layout;
-    pool->tile_bytes = tile;
-    const uint64_t tensor_bytes = static_cast<uint64_t>(tile) * static_cast<uint64_t>(desc->num_blocks);
-    for (uint64_t p : tab)
-        pool->spans.emplace_back(p, p + tensor_bytes);
-    std::sort(pool->spans.begin(), pool->spans.end());
-    for (size_t k = 1; k < pool->spans.size(); ++k) {
-        if (pool->spans[k].first < pool->spans[k - 1].second) { // layer tensors overlap each other
-            delete pool;
-            return LLMIG_EINVAL;
+    return no_throw([&]() -> int {
+        const int32_t L = desc->num_layers;
+        std::vector<uint64_t> tab(2 * static_cast<size_t>(L));
+        for (int32_t l = 0; l < L; ++l) {
+            tab[l] = desc->k_ptrs[l];
+            tab[L + l] = desc->v_ptrs[l];
         }
-    }
-    hipError_t e = hipGetDevice(&pool->device);
-    if (e == hipSuccess)
-        e = hipMalloc(reinterpret_cast<void **>(&pool->d_tab), tab.size() * sizeof(uint64_t));
-    if (e == hipSuccess)
-        e = hipMemcpy(pool->d_tab, tab.data(), tab.size() * sizeof(uint64_t), hipMemcpyHostToDevice);
-    if (e != hipSuccess) {
-        if (pool->d_tab)
-            (void)hipFree(pool->d_tab);
-        delete pool;
-        return hip_error(e);
-    }
-    *out = pool;
-    return LLMIG_OK;
+        for (uint64_t p : tab)
+            if (p == 0 || (p & 15u))
+                return LLMIG_EINVAL;
+
+        std::unique_ptr<llmig_pool> pool(new llmig_pool());
+        pool->num_layers = L;
+        pool->num_blocks = desc->num_blocks;
+        pool->block_size = desc->block_size;
+        pool->num_kv_heads = desc->num_kv_heads;
+        pool->head_dim = desc->head_dim;
+        pool->elem_bytes = desc->elem_bytes;
+        pool->layouts[0] = desc->k_layout;
+        pool->layouts[1] = desc->v_layout;
+        pool->tile_bytes = tile;
+        pool->d_tab = nullptr;
+        const uint64_t tensor_bytes = static_cast<uint64_t>(tile) * static_cast<uint64_t>(desc->num_blocks);
+        for (uint64_t p : tab)
+            pool->spans.emplace_back(p, p + tensor_bytes);
+        std::sort(pool->spans.begin(), pool->spans.end());
+        for (size_t k = 1; k < pool->spans.size(); ++k)
+            if (pool->spans[k].first < pool->spans[k - 1].second) // layer tensors overlap each other
+                return LLMIG_EINVAL;
+        hipError_t e = hipGetDevice(&pool->device);
+        if (e == hipSuccess)
+            e = hipMalloc(reinterpret_cast<void **>(&pool->d_tab), tab.size() * sizeof(uint64_t));
+        if (e == hipSuccess)
+            e = hipMemcpy(pool->d_tab, tab.data(), tab.size() * sizeof(uint64_t), hipMemcpyHostToDevice);
+        if (e != hipSuccess) {
+            if (pool->d_tab)
+                (void)hipFree(pool->d_tab);
+            return hip_error(e);
+        }
+        *out = pool.release();
+        return LLMIG_OK;
+    });
 }
 
 void llmig_pool_destroy(llmig_pool *pool)
@@ -434,57 +454,61 @@ int llmig_plan(const int32_t *src_table, int64_t src_table_len, const int32_t *d
                int64_t dst_free_len, int64_t len, int64_t from_tok, int64_t to_tok, int32_t block_size,
                int32_t *out_src, int32_t *out_dst, int64_t out_cap, int64_t *out_n)
 {
-    if (!out_n)
-        return LLMIG_EINVAL;
-    *out_n = 0;
-    if (block_size < 1 || len < 0 || from_tok < 0 || from_tok > to_tok || to_tok > len)
-        return LLMIG_EINVAL;
-    if (from_tok % block_size != 0 || (to_tok % block_size != 0 && to_tok != len))
-        return LLMIG_EINVAL;
-    if (src_table_len < 0 || dst_free_len < 0 || out_cap < 0)
-        return LLMIG_EINVAL;
-    const int64_t blocks_of_len = len / block_size + (len % block_size != 0);
-    if (src_table_len < blocks_of_len || (blocks_of_len > 0 && !src_table))
-        return LLMIG_EINVAL;
-    const int64_t first = from_tok / block_size;
-    const int64_t n = to_tok / block_size + (to_tok % block_size != 0) - first;
-    if (n > dst_free_len)
-        return LLMIG_ENOSPC;
-    if (n > out_cap || (n > 0 && (!dst_free_list || !out_src || !out_dst)))
-        return LLMIG_EINVAL;
-    const int32_t *src = src_table + first;
-    for (int64_t k = 0; k < n; ++k)
-        if (src[k] < 0 || dst_free_list[k] < 0)
-            return LLMIG_ERANGE;
-    if (has_repeat_any(src, n) || has_repeat_any(dst_free_list, n))
-        return LLMIG_EINVAL;
-    if (n > 0) { // the output arrays may be NULL for an empty stage
-        std::memcpy(out_src, src, static_cast<size_t>(n) * sizeof(int32_t));
-        std::memcpy(out_dst, dst_free_list, static_cast<size_t>(n) * sizeof(int32_t));
-    }
-    *out_n = n;
-    return LLMIG_OK;
+    return no_throw([&]() -> int {
+        if (!out_n)
+            return LLMIG_EINVAL;
+        *out_n = 0;
+        if (block_size < 1 || len < 0 || from_tok < 0 || from_tok > to_tok || to_tok > len)
+            return LLMIG_EINVAL;
+        if (from_tok % block_size != 0 || (to_tok % block_size != 0 && to_tok != len))
+            return LLMIG_EINVAL;
+        if (src_table_len < 0 || dst_free_len < 0 || out_cap < 0)
+            return LLMIG_EINVAL;
+        const int64_t blocks_of_len = len / block_size + (len % block_size != 0);
+        if (src_table_len < blocks_of_len || (blocks_of_len > 0 && !src_table))
+            return LLMIG_EINVAL;
+        const int64_t first = from_tok / block_size;
+        const int64_t n = to_tok / block_size + (to_tok % block_size != 0) - first;
+        if (n > dst_free_len)
+            return LLMIG_ENOSPC;
+        if (n > out_cap || (n > 0 && (!dst_free_list || !out_src || !out_dst)))
+            return LLMIG_EINVAL;
+        const int32_t *src = src_table + first;
+        for (int64_t k = 0; k < n; ++k)
+            if (src[k] < 0 || dst_free_list[k] < 0)
+                return LLMIG_ERANGE;
+        if (has_repeat_any(src, n) || has_repeat_any(dst_free_list, n))
+            return LLMIG_EINVAL;
+        if (n > 0) { // the output arrays may be NULL for an empty stage
+            std::memcpy(out_src, src, static_cast<size_t>(n) * sizeof(int32_t));
+            std::memcpy(out_dst, dst_free_list, static_cast<size_t>(n) * sizeof(int32_t));
+        }
+        *out_n = n;
+        return LLMIG_OK;
+    });
 }
 
 int llmig_stage(const llmig_pool *src, const llmig_pool *dst, const int32_t *map_src,
                 const int32_t *map_dst, int64_t n, int map_on_device, void *stream)
 {
-    if (!src || !dst || n < 0 || (map_on_device != 0 && map_on_device != 1))
-        return LLMIG_EINVAL;
-    if (!pools_compatible(src, dst))
-        return LLMIG_EINVAL;
-    if (n == 0)
-        return LLMIG_OK;
-    if (!map_src || !map_dst)
-        return LLMIG_EINVAL;
-    if (!map_on_device) {
-        int rc = check_pair_ids(src, dst, map_src, map_dst, n);
-        if (rc != LLMIG_OK)
-            return rc;
-        if (has_repeat(map_dst, n, dst->num_blocks))
+    return no_throw([&]() -> int {
+        if (!src || !dst || n < 0 || (map_on_device != 0 && map_on_device != 1))
             return LLMIG_EINVAL;
-    }
-    return launch_stage(src, dst, map_src, map_dst, n, map_on_device != 0, static_cast<hipStream_t>(stream));
+        if (!pools_compatible(src, dst))
+            return LLMIG_EINVAL;
+        if (n == 0)
+            return LLMIG_OK;
+        if (!map_src || !map_dst)
+            return LLMIG_EINVAL;
+        if (!map_on_device) {
+            int rc = check_pair_ids(src, dst, map_src, map_dst, n);
+            if (rc != LLMIG_OK)
+                return rc;
+            if (has_repeat(map_dst, n, dst->num_blocks))
+                return LLMIG_EINVAL;
+        }
+        return launch_stage(src, dst, map_src, map_dst, n, map_on_device != 0, static_cast<hipStream_t>(stream));
+    });
 }
 
 int llmig_migration_create(int32_t block_size, llmig_migration **out)
@@ -516,67 +540,75 @@ int llmig_migration_next(llmig_migration *m, const int32_t *src_table, int64_t s
                          int final_stage, const int32_t *dst_free_list, int64_t dst_free_len, int32_t *out_src,
                          int32_t *out_dst, int64_t out_cap, int64_t *out_n)
 {
-    if (!m || !out_n)
-        return LLMIG_EINVAL;
-    *out_n = 0;
-    int64_t from = 0, to = 0;
-    int rc = next_range(m, len, final_stage, &from, &to);
-    if (rc != LLMIG_OK)
-        return rc;
-    int64_t n = 0;
-    rc = llmig_plan(src_table, src_table_len, dst_free_list, dst_free_len, len, from, to, m->block_size, out_src,
-                    out_dst, out_cap, &n);
-    if (rc != LLMIG_OK)
-        return rc;
-    record_stage(m, out_dst, n, to, final_stage);
-    *out_n = n;
-    return LLMIG_OK;
+    return no_throw([&]() -> int {
+        if (!m || !out_n)
+            return LLMIG_EINVAL;
+        *out_n = 0;
+        int64_t from = 0, to = 0;
+        int rc = next_range(m, len, final_stage, &from, &to);
+        if (rc != LLMIG_OK)
+            return rc;
+        int64_t n = 0;
+        rc = llmig_plan(src_table, src_table_len, dst_free_list, dst_free_len, len, from, to, m->block_size, out_src,
+                        out_dst, out_cap, &n);
+        if (rc != LLMIG_OK)
+            return rc;
+        rc = record_stage(m, out_dst, n, to, final_stage);
+        if (rc != LLMIG_OK)
+            return rc;
+        *out_n = n;
+        return LLMIG_OK;
+    });
 }
 
 int llmig_migration_stage(llmig_migration *m, const llmig_pool *src, const llmig_pool *dst,
                           const int32_t *src_table, int64_t src_table_len, int64_t len, int final_stage,
                           const int32_t *dst_free_list, int64_t dst_free_len, void *stream, int64_t *out_n)
 {
-    if (!m || !out_n)
-        return LLMIG_EINVAL;
-    *out_n = 0;
-    const LaunchEvents ev = m->next_events; // this call's, whatever happens below
-    m->next_events = LaunchEvents();
-    if (!src || !dst || !pools_compatible(src, dst) || src->block_size != m->block_size)
-        return LLMIG_EINVAL;
-    int64_t from = 0, to = 0;
-    int rc = next_range(m, len, final_stage, &from, &to);
-    if (rc != LLMIG_OK)
-        return rc;
-    // Scratch for the stage's pairs: never more than the free list can give
-    // (a longer stage fails in llmig_plan before anything is written).
-    const int64_t bs = m->block_size;
-    const int64_t need = to / bs + (to % bs != 0) - from / bs;
-    if (need < 0 || dst_free_len < 0)
-        return LLMIG_EINVAL;
-    const size_t cap = static_cast<size_t>(std::max<int64_t>(std::min(need, dst_free_len), 1));
-    if (m->plan_src.size() < cap) {
-        try {
-            m->plan_src.resize(cap);
-            m->plan_dst.resize(cap);
-        } catch (...) {
+    return no_throw([&]() -> int {
+        if (!m || !out_n)
             return LLMIG_EINVAL;
+        *out_n = 0;
+        const LaunchEvents ev = m->next_events; // this call's, whatever happens below
+        m->next_events = LaunchEvents();
+        if (!src || !dst || !pools_compatible(src, dst) || src->block_size != m->block_size)
+            return LLMIG_EINVAL;
+        int64_t from = 0, to = 0;
+        int rc = next_range(m, len, final_stage, &from, &to);
+        if (rc != LLMIG_OK)
+            return rc;
+        // Scratch for the stage's pairs: never more than the free list can give
+        // (a longer stage fails in llmig_plan before anything is written).
+        const int64_t bs = m->block_size;
+        const int64_t need = to / bs + (to % bs != 0) - from / bs;
+        if (need < 0 || dst_free_len < 0)
+            return LLMIG_EINVAL;
+        const size_t cap = static_cast<size_t>(std::max<int64_t>(std::min(need, dst_free_len), 1));
+        if (m->plan_src.size() < cap) {
+            try {
+                m->plan_src.resize(cap);
+                m->plan_dst.resize(cap);
+            } catch (...) {
+                return LLMIG_EINVAL;
+            }
         }
-    }
-    int64_t n = 0;
-    rc = llmig_plan(src_table, src_table_len, dst_free_list, dst_free_len, len, from, to, m->block_size,
-                    m->plan_src.data(), m->plan_dst.data(), static_cast<int64_t>(cap), &n);
-    if (rc != LLMIG_OK)
-        return rc;
-    rc = check_pair_ids(src, dst, m->plan_src.data(), m->plan_dst.data(), n);
-    if (rc != LLMIG_OK)
-        return rc;
-    record_stage(m, m->plan_dst.data(), n, to, final_stage);
-    *out_n = n;
-    if (n == 0)
-        return LLMIG_OK;
-    return launch_stage(src, dst, m->plan_src.data(), m->plan_dst.data(), n, false,
-                        static_cast<hipStream_t>(stream), final_stage ? 0u : m->max_workgroups, ev);
+        int64_t n = 0;
+        rc = llmig_plan(src_table, src_table_len, dst_free_list, dst_free_len, len, from, to, m->block_size,
+                        m->plan_src.data(), m->plan_dst.data(), static_cast<int64_t>(cap), &n);
+        if (rc != LLMIG_OK)
+            return rc;
+        rc = check_pair_ids(src, dst, m->plan_src.data(), m->plan_dst.data(), n);
+        if (rc != LLMIG_OK)
+            return rc;
+        rc = record_stage(m, m->plan_dst.data(), n, to, final_stage);
+        if (rc != LLMIG_OK)
+            return rc;
+        *out_n = n;
+        if (n == 0)
+            return LLMIG_OK;
+        return launch_stage(src, dst, m->plan_src.data(), m->plan_dst.data(), n, false,
+                            static_cast<hipStream_t>(stream), final_stage ? 0u : m->max_workgroups, ev);
+    });
 }
 
 int llmig_migration_set_stage_events(llmig_migration *m, void *start_event, void *stop_event)
@@ -650,74 +682,80 @@ int llmig_migration_info(const llmig_migration *m, int32_t *state, int64_t *copi
 int llmig_pack(const llmig_pool *src, const int32_t *blocks, int64_t n, int map_on_device,
                void *staging, int64_t staging_bytes, void *stream)
 {
-    int rc = fused_copy_checks(src, blocks, n, map_on_device, staging, staging_bytes, false);
-    if (rc != LLMIG_OK || n == 0)
-        return rc;
-    void *lin = nullptr;
-    rc = staging_pointer(staging, &lin);
-    if (rc != LLMIG_OK)
-        return rc;
-    CopyArgs a;
-    std::memset(&a, 0, sizeof(a));
-    a.src_tab = src->d_tab;
-    a.dst_lin = static_cast<uint8_t *>(lin);
-    a.tile_bytes = static_cast<uint32_t>(src->tile_bytes);
-    a.num_layers = static_cast<uint32_t>(src->num_layers);
-    return launch_copy<kPool, kLinear>(a, blocks, nullptr, n, map_on_device != 0,
-                                       static_cast<hipStream_t>(stream));
+    return no_throw([&]() -> int {
+        int rc = fused_copy_checks(src, blocks, n, map_on_device, staging, staging_bytes, false);
+        if (rc != LLMIG_OK || n == 0)
+            return rc;
+        void *lin = nullptr;
+        rc = staging_pointer(staging, &lin);
+        if (rc != LLMIG_OK)
+            return rc;
+        CopyArgs a;
+        std::memset(&a, 0, sizeof(a));
+        a.src_tab = src->d_tab;
+        a.dst_lin = static_cast<uint8_t *>(lin);
+        a.tile_bytes = static_cast<uint32_t>(src->tile_bytes);
+        a.num_layers = static_cast<uint32_t>(src->num_layers);
+        return launch_copy<kPool, kLinear>(a, blocks, nullptr, n, map_on_device != 0,
+                                           static_cast<hipStream_t>(stream));
+    });
 }
 
 int llmig_unpack(const llmig_pool *dst, const int32_t *blocks, int64_t n, int map_on_device,
                  const void *staging, int64_t staging_bytes, void *stream)
 {
-    int rc = fused_copy_checks(dst, blocks, n, map_on_device, staging, staging_bytes, true);
-    if (rc != LLMIG_OK || n == 0)
-        return rc;
-    void *lin = nullptr;
-    rc = staging_pointer(staging, &lin);
-    if (rc != LLMIG_OK)
-        return rc;
-    CopyArgs a;
-    std::memset(&a, 0, sizeof(a));
-    a.dst_tab = dst->d_tab;
-    a.src_lin = static_cast<const uint8_t *>(lin);
-    a.tile_bytes = static_cast<uint32_t>(dst->tile_bytes);
-    a.num_layers = static_cast<uint32_t>(dst->num_layers);
-    return launch_copy<kLinear, kPool>(a, nullptr, blocks, n, map_on_device != 0,
-                                       static_cast<hipStream_t>(stream));
+    return no_throw([&]() -> int {
+        int rc = fused_copy_checks(dst, blocks, n, map_on_device, staging, staging_bytes, true);
+        if (rc != LLMIG_OK || n == 0)
+            return rc;
+        void *lin = nullptr;
+        rc = staging_pointer(staging, &lin);
+        if (rc != LLMIG_OK)
+            return rc;
+        CopyArgs a;
+        std::memset(&a, 0, sizeof(a));
+        a.dst_tab = dst->d_tab;
+        a.src_lin = static_cast<const uint8_t *>(lin);
+        a.tile_bytes = static_cast<uint32_t>(dst->tile_bytes);
+        a.num_layers = static_cast<uint32_t>(dst->num_layers);
+        return launch_copy<kLinear, kPool>(a, nullptr, blocks, n, map_on_device != 0,
+                                           static_cast<hipStream_t>(stream));
+    });
 }
 
 int llmig_unpack_layout(const llmig_pool *dst, const int32_t *blocks, int64_t n, int map_on_device,
                         const void *staging, int64_t staging_bytes, int32_t staging_k_layout,
                         int32_t staging_v_layout, void *stream)
 {
-    const int32_t from[2] = {staging_k_layout, staging_v_layout};
-    for (int32_t layout : from)
-        if (layout < LLMIG_LAYOUT_NHD || layout > LLMIG_LAYOUT_HDN)
+    return no_throw([&]() -> int {
+        const int32_t from[2] = {staging_k_layout, staging_v_layout};
+        for (int32_t layout : from)
+            if (layout < LLMIG_LAYOUT_NHD || layout > LLMIG_LAYOUT_HDN)
+                return LLMIG_EINVAL;
+        if (dst && from[0] == dst->layouts[0] && from[1] == dst->layouts[1])
+            return llmig_unpack(dst, blocks, n, map_on_device, staging, staging_bytes, stream);
+        int rc = fused_copy_checks(dst, blocks, n, map_on_device, staging, staging_bytes, true);
+        if (rc != LLMIG_OK)
+            return rc;
+        if (!conversion_supported(dst, from))
             return LLMIG_EINVAL;
-    if (dst && from[0] == dst->layouts[0] && from[1] == dst->layouts[1])
-        return llmig_unpack(dst, blocks, n, map_on_device, staging, staging_bytes, stream);
-    int rc = fused_copy_checks(dst, blocks, n, map_on_device, staging, staging_bytes, true);
-    if (rc != LLMIG_OK)
-        return rc;
-    if (!conversion_supported(dst, from))
-        return LLMIG_EINVAL;
-    if (n == 0)
-        return LLMIG_OK;
-    void *lin = nullptr;
-    rc = staging_pointer(staging, &lin);
-    if (rc != LLMIG_OK)
-        return rc;
-    ConvertArgs c = convert_args(dst, from, dst->layouts);
-    c.src_lin = static_cast<const uint8_t *>(lin);
-    c.dst_tab = dst->d_tab;
-    return launch_convert(c, nullptr, blocks, n, map_on_device != 0, static_cast<hipStream_t>(stream), 0);
+        if (n == 0)
+            return LLMIG_OK;
+        void *lin = nullptr;
+        rc = staging_pointer(staging, &lin);
+        if (rc != LLMIG_OK)
+            return rc;
+        ConvertArgs c = convert_args(dst, from, dst->layouts);
+        c.src_lin = static_cast<const uint8_t *>(lin);
+        c.dst_tab = dst->d_tab;
+        return launch_convert(c, nullptr, blocks, n, map_on_device != 0, static_cast<hipStream_t>(stream), 0);
+    });
 }
 
 int llmig_write_tokens(const llmig_pool *pool, const int32_t *table, int64_t table_len, int64_t from_tok,
                        int64_t n_tok, const void *data, void *stream)
 {
-    if (!pool || from_tok < 0 || n_tok < 0 || table_len < 0)
+    if (!pool || from_tok < 0 || n_tok < 0 || table_len < 0 || from_tok > INT64_MAX - n_tok)
         return LLMIG_EINVAL;
     if (n_tok == 0)
         return LLMIG_OK;
@@ -802,96 +840,113 @@ static int attn_items(const int32_t *ctx_lens, int32_t batch, std::vector<int32_
     return LLMIG_OK;
 }
 
+// Workspace of a decode-attention call: per layer, item and query head, the
+// partial output (head_dim floats), its running maximum and its sum.
+static int attn_workspace_bytes(int64_t num_layers, int64_t n_items, int64_t q_heads, int64_t head_dim,
+                                int64_t *bytes)
+{
+    int64_t v = 0;
+    if (__builtin_mul_overflow(num_layers, n_items, &v) || __builtin_mul_overflow(v, q_heads, &v) ||
+        __builtin_mul_overflow(v, (head_dim + 2) * 4, &v))
+        return LLMIG_EINVAL;
+    *bytes = v;
+    return LLMIG_OK;
+}
+
 int llmig_decode_attention_workspace(const int32_t *ctx_lens, int32_t batch, int32_t num_layers, int32_t q_heads,
                                      int32_t head_dim, int64_t *bytes)
 {
-    if (!bytes)
-        return LLMIG_EINVAL;
-    *bytes = 0;
-    if (!ctx_lens || batch < 1 || batch > kAttnMaxBatch || num_layers < 1 || q_heads < 1 || head_dim < 1)
-        return LLMIG_EINVAL;
-    std::vector<int32_t> seq, start, end;
-    if (attn_items(ctx_lens, batch, seq, start, end) != LLMIG_OK)
-        return LLMIG_EINVAL;
-    *bytes = static_cast<int64_t>(num_layers) * static_cast<int64_t>(seq.size()) * q_heads * (head_dim + 2) * 4;
-    return LLMIG_OK;
+    return no_throw([&]() -> int {
+        if (!bytes)
+            return LLMIG_EINVAL;
+        *bytes = 0;
+        if (!ctx_lens || batch < 1 || batch > kAttnMaxBatch || num_layers < 1 || q_heads < 1 || head_dim < 1)
+            return LLMIG_EINVAL;
+        std::vector<int32_t> seq, start, end;
+        if (attn_items(ctx_lens, batch, seq, start, end) != LLMIG_OK)
+            return LLMIG_EINVAL;
+        return attn_workspace_bytes(num_layers, static_cast<int64_t>(seq.size()), q_heads, head_dim, bytes);
+    });
 }
 
 int llmig_decode_attention(const llmig_pool *pool, int32_t dtype, const void *q, int32_t batch, int32_t q_heads,
                            const int32_t *tables, int32_t table_stride, const int32_t *ctx_lens, float scale,
                            void *workspace, int64_t workspace_bytes, float *out, void *stream)
 {
-    if (!pool || (dtype != 0 && dtype != 1) || pool->elem_bytes != 2 || !q || !tables || !ctx_lens || !out ||
-        batch < 1 || batch > kAttnMaxBatch || q_heads < 1 || table_stride < 1 ||
-        pool->layouts[0] != LLMIG_LAYOUT_NHD || pool->layouts[1] != LLMIG_LAYOUT_NHD)
-        return LLMIG_EINVAL;
-    const int32_t D = pool->head_dim, hkv = pool->num_kv_heads;
-    if (q_heads % hkv != 0)
-        return LLMIG_EINVAL;
-    const void *fn = attn_kernel_for(dtype, D, q_heads / hkv);
-    if (!fn || (reinterpret_cast<uintptr_t>(q) & 15u) || (reinterpret_cast<uintptr_t>(out) & 3u) ||
-        (reinterpret_cast<uintptr_t>(tables) & 3u) || (reinterpret_cast<uintptr_t>(workspace) & 3u))
-        return LLMIG_EINVAL;
-    for (int32_t b = 0; b < batch; ++b)
-        if (ctx_lens[b] < 0 || (ctx_lens[b] + pool->block_size - 1) / pool->block_size > table_stride)
+    return no_throw([&]() -> int {
+        if (!pool || (dtype != 0 && dtype != 1) || pool->elem_bytes != 2 || !q || !tables || !ctx_lens || !out ||
+            batch < 1 || batch > kAttnMaxBatch || q_heads < 1 || table_stride < 1 ||
+            pool->layouts[0] != LLMIG_LAYOUT_NHD || pool->layouts[1] != LLMIG_LAYOUT_NHD)
             return LLMIG_EINVAL;
-    std::vector<int32_t> seq, start, end;
-    if (attn_items(ctx_lens, batch, seq, start, end) != LLMIG_OK)
-        return LLMIG_EINVAL;
-    const int64_t n_items = static_cast<int64_t>(seq.size());
-    const int64_t need = static_cast<int64_t>(pool->num_layers) * n_items * q_heads * (D + 2) * 4;
-    if (n_items > 0 && (!workspace || workspace_bytes < need))
-        return LLMIG_EINVAL;
-    hipStream_t st = static_cast<hipStream_t>(stream);
+        const int32_t D = pool->head_dim, hkv = pool->num_kv_heads;
+        if (q_heads % hkv != 0)
+            return LLMIG_EINVAL;
+        const void *fn = attn_kernel_for(dtype, D, q_heads / hkv);
+        if (!fn || (reinterpret_cast<uintptr_t>(q) & 15u) || (reinterpret_cast<uintptr_t>(out) & 3u) ||
+            (reinterpret_cast<uintptr_t>(tables) & 3u) || (reinterpret_cast<uintptr_t>(workspace) & 3u))
+            return LLMIG_EINVAL;
+        for (int32_t b = 0; b < batch; ++b)
+            if (ctx_lens[b] < 0 || (ctx_lens[b] + pool->block_size - 1) / pool->block_size > table_stride)
+                return LLMIG_EINVAL;
+        std::vector<int32_t> seq, start, end;
+        if (attn_items(ctx_lens, batch, seq, start, end) != LLMIG_OK)
+            return LLMIG_EINVAL;
+        const int64_t n_items = static_cast<int64_t>(seq.size());
+        int64_t need = 0;
+        if (attn_workspace_bytes(pool->num_layers, n_items, q_heads, D, &need) != LLMIG_OK ||
+            n_items > 0x7fffffffLL || (n_items > 0 && (!workspace || workspace_bytes < need)))
+            return LLMIG_EINVAL;
+        hipStream_t st = static_cast<hipStream_t>(stream);
 
-    AttnArgs a;
-    std::memset(&a, 0, sizeof(a));
-    a.k_tab = pool->d_tab;
-    a.q = static_cast<const uint8_t *>(q);
-    a.tables = tables;
-    a.ws = static_cast<float *>(workspace);
-    a.scale = scale;
-    a.num_layers = static_cast<uint32_t>(pool->num_layers);
-    a.batch = static_cast<uint32_t>(batch);
-    a.q_heads = static_cast<uint32_t>(q_heads);
-    a.kv_heads = static_cast<uint32_t>(hkv);
-    a.block_size = static_cast<uint32_t>(pool->block_size);
-    a.table_stride = static_cast<uint32_t>(table_stride);
-    a.n_items_total = static_cast<uint32_t>(n_items);
-    for (int64_t first = 0; first < n_items; first += kAttnItems) {
-        const int64_t m = std::min<int64_t>(kAttnItems, n_items - first);
-        a.item_base = static_cast<uint32_t>(first);
-        a.items = static_cast<uint32_t>(m);
-        std::memcpy(a.item_seq, seq.data() + first, m * sizeof(int32_t));
-        std::memcpy(a.item_start, start.data() + first, m * sizeof(int32_t));
-        std::memcpy(a.item_end, end.data() + first, m * sizeof(int32_t));
-        void *args[] = {&a};
-        hipError_t e = hipLaunchKernel(fn, dim3(static_cast<uint32_t>(m * hkv), a.num_layers), dim3(kThreads), args,
-                                       0, st);
-        if (e != hipSuccess)
-            return hip_error(e);
-    }
-    AttnReduceArgs r;
-    std::memset(&r, 0, sizeof(r));
-    r.ws = static_cast<const float *>(workspace);
-    r.out = out;
-    r.num_layers = a.num_layers;
-    r.batch = a.batch;
-    r.q_heads = a.q_heads;
-    r.head_dim = static_cast<uint32_t>(D);
-    r.n_items_total = a.n_items_total;
-    for (int64_t i = 0, b = 0; b < batch; ++b) {
-        r.seq_first[b] = static_cast<int32_t>(i);
-        while (i < n_items && seq[i] == b)
-            ++i;
-        r.seq_count[b] = static_cast<int32_t>(i) - r.seq_first[b];
-    }
-    const uint64_t total = static_cast<uint64_t>(pool->num_layers) * batch * q_heads * D;
-    const uint32_t grid = static_cast<uint32_t>(std::min<uint64_t>((total + kThreads - 1) / kThreads, 1u << 20));
-    void *rargs[] = {&r};
-    hipError_t e = hipLaunchKernel(reinterpret_cast<const void *>(&attn_reduce), dim3(grid), dim3(kThreads), rargs, 0,
-                                   st);
-    return e == hipSuccess ? LLMIG_OK : hip_error(e);
+        AttnArgs a;
+        std::memset(&a, 0, sizeof(a));
+        a.k_tab = pool->d_tab;
+        a.q = static_cast<const uint8_t *>(q);
+        a.tables = tables;
+        a.ws = static_cast<float *>(workspace);
+        a.scale = scale;
+        a.num_layers = static_cast<uint32_t>(pool->num_layers);
+        a.batch = static_cast<uint32_t>(batch);
+        a.q_heads = static_cast<uint32_t>(q_heads);
+        a.kv_heads = static_cast<uint32_t>(hkv);
+        a.block_size = static_cast<uint32_t>(pool->block_size);
+        a.table_stride = static_cast<uint32_t>(table_stride);
+        a.n_items_total = static_cast<uint32_t>(n_items);
+        for (int64_t first = 0; first < n_items; first += kAttnItems) {
+            const int64_t m = std::min<int64_t>(kAttnItems, n_items - first);
+            a.item_base = static_cast<uint32_t>(first);
+            a.items = static_cast<uint32_t>(m);
+            std::memcpy(a.item_seq, seq.data() + first, m * sizeof(int32_t));
+            std::memcpy(a.item_start, start.data() + first, m * sizeof(int32_t));
+            std::memcpy(a.item_end, end.data() + first, m * sizeof(int32_t));
+            void *args[] = {&a};
+            hipError_t e = hipLaunchKernel(fn, dim3(static_cast<uint32_t>(m * hkv), a.num_layers), dim3(kThreads), args,
+                                           0, st);
+            if (e != hipSuccess)
+                return hip_error(e);
+        }
+        AttnReduceArgs r;
+        std::memset(&r, 0, sizeof(r));
+        r.ws = static_cast<const float *>(workspace);
+        r.out = out;
+        r.num_layers = a.num_layers;
+        r.batch = a.batch;
+        r.q_heads = a.q_heads;
+        r.head_dim = static_cast<uint32_t>(D);
+        r.n_items_total = a.n_items_total;
+        for (int64_t i = 0, b = 0; b < batch; ++b) {
+            r.seq_first[b] = static_cast<int32_t>(i);
+            while (i < n_items && seq[i] == b)
+                ++i;
+            r.seq_count[b] = static_cast<int32_t>(i) - r.seq_first[b];
+        }
+        const uint64_t total = static_cast<uint64_t>(pool->num_layers) * batch * q_heads * D;
+        const uint32_t grid = static_cast<uint32_t>(std::min<uint64_t>((total + kThreads - 1) / kThreads, 1u << 20));
+        void *rargs[] = {&r};
+        hipError_t e = hipLaunchKernel(reinterpret_cast<const void *>(&attn_reduce), dim3(grid), dim3(kThreads), rargs, 0,
+                                       st);
+        return e == hipSuccess ? LLMIG_OK : hip_error(e);
+    });
 }
 
 const char *llmig_strerror(int code)

@@ -323,13 +323,18 @@ class MigrationHandle:
     def stage(self, src: "Pool", dst: "Pool", src_table: np.ndarray, length: int, final: bool,
               dst_free_list: np.ndarray, stream=None) -> int:
         """Plan, reserve and launch the next stage; returns the number of
-        free-list entries consumed."""
+        free-list entries consumed.  A HIP error after the reservation
+        raises with ``consumed`` set to the entries reserved all the same
+        (an abort returns them); other errors consume nothing."""
         st, fl = _host_i32(src_table), _host_i32(dst_free_list)
         n = ctypes.c_int64(0)
-        _check(_lib.llmig_migration_stage(self._h, src.handle, dst.handle, st.ctypes.data, st.size,
+        code = _lib.llmig_migration_stage(self._h, src.handle, dst.handle, st.ctypes.data, st.size,
                                           int(length), int(bool(final)), fl.ctypes.data,
-                                          fl.size, _stream(stream), ctypes.byref(n)),
-               "llmig_migration_stage")
+                                          fl.size, _stream(stream), ctypes.byref(n))
+        if code != LLMIG_OK:
+            err = LlmigError(code, "llmig_migration_stage")
+            err.consumed = n.value
+            raise err
         return n.value
 
     def _take(self, fn, where):

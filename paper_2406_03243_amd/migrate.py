@@ -23,7 +23,7 @@ from dataclasses import dataclass
 import numpy as np
 import torch
 
-from .llmig import MigrationHandle, Pool, llmig_pack, llmig_plan, llmig_unpack, llmig_write_tokens
+from .llmig import LlmigError, MigrationHandle, Pool, llmig_pack, llmig_plan, llmig_unpack, llmig_write_tokens
 
 
 # Timing event pairs whose times have been read, kept for the next stages:
@@ -92,7 +92,11 @@ class Migration:
             # without the host work that plans and checks the stage
             ev = _timer_pair()
             self.coord.set_stage_events(*ev)
-        n = self.coord.stage(self.src, self.dst, self.src_table, length, final, self.free, stream=self.stream)
+        try:
+            n = self.coord.stage(self.src, self.dst, self.src_table, length, final, self.free, stream=self.stream)
+        except LlmigError as e:
+            self._consumed += getattr(e, "consumed", 0)   # reserved before a HIP failure: abort returns them
+            raise
         if time_it and n == 0:
             _spare_timers.append(ev)    # not recorded by the library: free again
             ev = None
