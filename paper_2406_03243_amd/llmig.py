@@ -148,8 +148,10 @@ class Pool:
         t0 = k_layers[0]
         for t in list(k_layers) + list(v_layers):
             if (not t.is_cuda or not t.is_contiguous() or t.dim() != 4 or t.shape != t0.shape
-                    or t.dtype != t0.dtype):
-                raise ValueError("layer tensors must be contiguous CUDA tensors of one 4-D shape and dtype")
+                    or t.dtype != t0.dtype or t.device != t0.device):
+                raise ValueError("layer tensors must be contiguous CUDA tensors of one 4-D shape, dtype and device")
+        if t0.device.index != torch.cuda.current_device():
+            raise ValueError("register a pool with its device current")
         nb, bs, heads, dim = t0.shape
         kp = (ctypes.c_uint64 * len(k_layers))(*[t.data_ptr() for t in k_layers])
         vp = (ctypes.c_uint64 * len(v_layers))(*[t.data_ptr() for t in v_layers])
@@ -368,11 +370,17 @@ def llmig_decode_attention(pool: Pool, q: torch.Tensor, tables: torch.Tensor, ct
     lengths; out: CUDA float32 [L][B][Hq][D]."""
     if q.dtype not in (torch.float16, torch.bfloat16) or not q.is_cuda or not q.is_contiguous():
         raise ValueError("q must be a contiguous CUDA fp16/bf16 tensor")
+    if q.dim() != 4 or q.shape[0] != pool.num_layers or q.shape[3] != pool.head_dim or q.dtype != pool.k[0].dtype:
+        raise ValueError("q must be [num_layers][batch][q_heads][head_dim] of the pool's layers and type")
     if tables.dtype != torch.int32 or not tables.is_cuda or not tables.is_contiguous() or tables.dim() != 2:
         raise ValueError("tables must be a contiguous CUDA int32 [batch][stride] tensor")
     if out.dtype != torch.float32 or not out.is_cuda or not out.is_contiguous() or out.shape != q.shape:
         raise ValueError("out must be a contiguous CUDA float32 tensor shaped like q")
+    if not workspace.is_cuda or not workspace.is_contiguous():
+        raise ValueError("workspace must be a contiguous CUDA tensor")
     c = _host_i32(ctx_lens)
+    if c.size != q.shape[1] or tables.shape[0] < q.shape[1]:
+        raise ValueError("ctx_lens must hold one length per sequence of q, tables one row each")
     _check(_lib.llmig_decode_attention(pool.handle, 1 if q.dtype == torch.bfloat16 else 0, q.data_ptr(),
                                        q.shape[1], q.shape[2], tables.data_ptr(), tables.shape[1],
                                        c.ctypes.data, float(scale), workspace.data_ptr(),
@@ -383,8 +391,9 @@ def llmig_decode_attention(pool: Pool, q: torch.Tensor, tables: torch.Tensor, ct
 def llmig_stream_read(region: torch.Tensor, passes: int, workgroups: int, out: torch.Tensor, stream=None) -> None:
     """Harness: read ``region`` ``passes`` times on ``workgroups`` workgroups
     (decode stand-in); ``out`` is a CUDA int64 tensor of workgroups * 256."""
-    if not region.is_cuda or not out.is_cuda or out.dtype != torch.int64:
-        raise ValueError("region and out must be CUDA tensors, out int64")
+    if (not region.is_cuda or not out.is_cuda or out.dtype != torch.int64 or not region.is_contiguous()
+            or not out.is_contiguous()):
+        raise ValueError("region and out must be contiguous CUDA tensors, out int64")
     _check(_lib.llmig_stream_read(region.data_ptr(), region.numel() * region.element_size(), int(passes),
                                   int(workgroups), out.data_ptr(), out.numel(), _stream(stream)),
            "llmig_stream_read")

@@ -107,5 +107,18 @@ def test_decode_attention_rejects_unsupported():
         llmig_decode_attention(pool, q, tab, [40], 1.0, ws, out)
     with pytest.raises(LlmigError):                      # workspace too small
         llmig_decode_attention(pool, q, tab, [10], 1.0, ws[:16], out)
+    bad_q = [torch.zeros((2, 1, 4, 64), dtype=torch.float16, device="cuda"),   # layers
+             torch.zeros((1, 1, 4, 128), dtype=torch.float16, device="cuda"),  # head_dim
+             torch.zeros((1, 1, 4, 64), dtype=torch.bfloat16, device="cuda")]  # type
+    for bq in bad_q:
+        with pytest.raises(ValueError):
+            llmig_decode_attention(pool, bq, tab, [10], 1.0, ws, torch.zeros(bq.shape, dtype=torch.float32,
+                                                                             device="cuda"))
+    with pytest.raises(ValueError):                      # one length per sequence
+        llmig_decode_attention(pool, q, tab, [10, 10], 1.0, ws, out)
+    with pytest.raises(ValueError):                      # a table row per sequence
+        q2 = torch.zeros((1, 2, 4, 64), dtype=torch.float16, device="cuda")
+        llmig_decode_attention(pool, q2, tab, [10, 10], 1.0, ws, torch.zeros(q2.shape, dtype=torch.float32,
+                                                                              device="cuda"))
     llmig_decode_attention(pool, q, tab, [10], 1.0, ws, out)
     torch.cuda.synchronize()
