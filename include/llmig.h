@@ -102,7 +102,12 @@ typedef struct llmig_pool llmig_pool;
  * copies the per-layer address table to device memory once.  The library
  * owns only that table; the pool memory stays the caller's and must outlive
  * the handle.  Errors: LLMIG_EINVAL (a non-positive size, a null array or
- * address, misalignment, a tile over 2^31 bytes), LLMIG_EHIP. */
+ * address, misalignment, a tile over 2^31 bytes), LLMIG_EHIP.
+ *
+ * Every call that enqueues work on a pool (stage, pack, unpack, write_tokens,
+ * decode attention, the coordinator's stage) must be made with the pool's
+ * device current, else LLMIG_EINVAL, and on a stream of that device (not
+ * checked). */
 int llmig_pool_create(const llmig_pool_desc *desc, llmig_pool **out);
 
 /* Frees the handle and its device table (not the pool memory).  The caller

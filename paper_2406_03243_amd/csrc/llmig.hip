@@ -154,6 +154,14 @@ int no_throw(Body &&body)
     }
 }
 
+// Whether the pool lives on the calling thread's current device, where the
+// library launches its kernels.
+bool on_current_device(const llmig_pool *pool)
+{
+    int d = -1;
+    return hipGetDevice(&d) == hipSuccess && d == pool->device;
+}
+
 bool same_geometry(const llmig_pool *a, const llmig_pool *b)
 {
     return a->num_layers == b->num_layers && a->block_size == b->block_size &&
@@ -251,7 +259,7 @@ int staging_pointer(const void *p, void **out)
 int fused_copy_checks(const llmig_pool *pool, const int32_t *blocks, int64_t n, int map_on_device,
                       const void *staging, int64_t staging_bytes, bool reject_repeats)
 {
-    if (!pool || n < 0 || (map_on_device != 0 && map_on_device != 1))
+    if (!pool || n < 0 || (map_on_device != 0 && map_on_device != 1) || !on_current_device(pool))
         return LLMIG_EINVAL;
     if (n == 0)
         return LLMIG_OK;
@@ -310,8 +318,8 @@ ConvertArgs convert_args(const llmig_pool *pool, const int32_t *src_layouts, con
 
 bool pools_compatible(const llmig_pool *src, const llmig_pool *dst)
 {
-    return same_geometry(src, dst) && src->device == dst->device && !pools_overlap(src, dst) &&
-           (same_layouts(src, dst) || conversion_supported(src, dst->layouts));
+    return same_geometry(src, dst) && src->device == dst->device && on_current_device(src) &&
+           !pools_overlap(src, dst) && (same_layouts(src, dst) || conversion_supported(src, dst->layouts));
 }
 
 int check_pair_ids(const llmig_pool *src, const llmig_pool *dst, const int32_t *ms, const int32_t *md, int64_t n)
@@ -755,7 +763,8 @@ int llmig_unpack_layout(const llmig_pool *dst, const int32_t *blocks, int64_t n,
 int llmig_write_tokens(const llmig_pool *pool, const int32_t *table, int64_t table_len, int64_t from_tok,
                        int64_t n_tok, const void *data, void *stream)
 {
-    if (!pool || from_tok < 0 || n_tok < 0 || table_len < 0 || from_tok > INT64_MAX - n_tok)
+    if (!pool || from_tok < 0 || n_tok < 0 || table_len < 0 || from_tok > INT64_MAX - n_tok ||
+        !on_current_device(pool))
         return LLMIG_EINVAL;
     if (n_tok == 0)
         return LLMIG_OK;
@@ -874,7 +883,8 @@ int llmig_decode_attention(const llmig_pool *pool, int32_t dtype, const void *q,
                            void *workspace, int64_t workspace_bytes, float *out, void *stream)
 {
     return no_throw([&]() -> int {
-        if (!pool || (dtype != 0 && dtype != 1) || pool->elem_bytes != 2 || !q || !tables || !ctx_lens || !out ||
+        if (!pool || !on_current_device(pool) || (dtype != 0 && dtype != 1) || pool->elem_bytes != 2 || !q ||
+            !tables || !ctx_lens || !out ||
             batch < 1 || batch > kAttnMaxBatch || q_heads < 1 || table_stride < 1 ||
             pool->layouts[0] != LLMIG_LAYOUT_NHD || pool->layouts[1] != LLMIG_LAYOUT_NHD)
             return LLMIG_EINVAL;
