@@ -32,6 +32,7 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0  # MI355X HBM3E, published
+PCIE_GBS = 64.0        # PCIe Gen5 x16, per direction
 
 
 def log(*a):
@@ -403,7 +404,7 @@ def batched_section(reps=20, host_reps=3, chunk_pairs=64):
     """64 requests migrated in one llmig_stage call; the same pairs packed
     into and unpacked from device staging (block fusion's kernels alone);
     and the same pairs through pinned host memory (pack -> host -> unpack,
-    chunked, two buffers)."""
+    chunked, two buffers), then each direction alone."""
     import torch
 
     from paper_2406_03243_amd import harness, migrate, scenarios
@@ -477,6 +478,31 @@ def batched_section(reps=20, host_reps=3, chunk_pairs=64):
                 host_times.append(time.perf_counter() - t0)
         ht = statistics.median(host_times)
         out["host_staged"][mode] = {"seconds_median": round(ht, 4), "GBps_each_way": round(one_way / ht / 1e9, 2)}
+
+    # One direction at a time (the link each side of a two-GPU migration
+    # would carry alone): every chunk packed into the pinned buffers, then
+    # every chunk unpacked from them.
+    def one_direction(pack: bool) -> float:
+        times = []
+        for r in range(host_reps + 1):
+            torch.cuda.synchronize()
+            t0 = time.perf_counter()
+            for c, lo in enumerate(range(0, len(ms), chunk_pairs)):
+                if pack:
+                    llmig_pack(src, ms[lo:lo + chunk_pairs], bufs[c % 2], stream=ps)
+                else:
+                    llmig_unpack(dst, md[lo:lo + chunk_pairs], bufs[c % 2], stream=us_)
+            torch.cuda.synchronize()
+            if r:
+                times.append(time.perf_counter() - t0)
+        return statistics.median(times)
+
+    for name, pack in (("pack_to_host_alone", True), ("unpack_from_host_alone", False)):
+        t = one_direction(pack)
+        gbs = one_way / t / 1e9
+        out["host_staged"][name] = {"seconds_median": round(t, 4), "GBps": round(gbs, 2),
+                                    "link_frac": round(gbs / PCIE_GBS, 3)}
+    log("batched host staged", out["host_staged"])
     su.close()
     return out
 
