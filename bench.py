@@ -65,16 +65,12 @@ def recorded_traffic(kernel: str):
 
 
 def bulk_span_rows(tile_bytes: int) -> int:
-    """The copy kernel instance (SPAN, in 1 KiB rows per wavefront) of a bulk
-    launch: a tile is cut into four equal spans (more when a span would pass
-    32 rows) and the instance is the power of two at or above the span,
-    within [2, 32] (mirrors the library's launch configuration, for
-    labelling only)."""
-    rows = -(-tile_bytes // 1024)
-    spans = max(min(4, rows), -(-rows // 32))
-    span_rows = -(-rows // spans)
+    """The copy kernel's span (1 KiB rows per wavefront) for a bulk launch:
+    the power of two at or above a quarter of the tile, within [2, 32]
+    (mirrors the library's launch configuration, for labelling only)."""
+    quarter = -(-tile_bytes // 4096)
     span = 2
-    while span < 32 and span < span_rows:
+    while span < 32 and span < quarter:
         span *= 2
     return span
 
@@ -201,6 +197,14 @@ def main():
     downtimes = [d for _, d in runs]
     kernel_name = "copy_tiles<0, 0, %d, %d>" % (ids_mode, bulk_span_rows(src.tile_bytes))
 
+    # GPU time of the final stage's copy alone (events around its launch), in
+    # extra steps outside the timed region: the host downtime above also
+    # holds its planning, launch and the host's view of completion.
+    final_gpu = []
+    for _ in range(max(args.steps, 10)):
+        mf, _ = migrate.run_scheduled(src, dst, table, free, initial, appends, mig, dec, time_final=True)
+        final_gpu.append(mf.stages[-1].gpu_us)
+
     stages = []
     for i, rec in enumerate(m0.stages):
         us = [m.stages[i].gpu_us for m, _ in runs if m.stages[i].gpu_us > 0]
@@ -250,6 +254,7 @@ def main():
                           "source": "Llumnix section 6.2"},
         "final_stage_downtime_us": {"median": round(statistics.median(downtimes), 1),
                                     "min": round(min(downtimes), 1), "max": round(max(downtimes), 1)},
+        "final_stage_gpu_us": spread(final_gpu),
     }
 
     # ------------------------------------------------------------------ CPU oracle baseline
@@ -373,6 +378,12 @@ def downtime_sweep(reps):
             m, dt = migrate.run_timed(src, dst, table, length, free, append_pool, mig, dec, step_ms=20.0)
             if r:
                 res.append((m, dt))
+        # the final stage's GPU time alone (events around its launch)
+        final_gpu = []
+        for r in range(reps):
+            m, _ = migrate.run_timed(src, dst, table, length, free, append_pool, mig, dec, step_ms=20.0,
+                                     time_final=True)
+            final_gpu.append(m.stages[-1].gpu_us)
         # blocking copy: the whole request as one stage, all of it downtime
         blocking = []
         for r in range(reps + 1):
@@ -394,6 +405,7 @@ def downtime_sweep(reps):
             "final_blocks": res[0][0].stages[-1].blocks,
             "downtime_us_median": round(statistics.median(dt for _, dt in res), 1),
             "downtime_us_min": round(min(dt for _, dt in res), 1),
+            "final_stage_gpu_us_median": round(statistics.median(final_gpu), 1),
             "blocking_copy_downtime_us_median": round(statistics.median(blocking), 1),
         }
     su.close()

@@ -10,19 +10,15 @@
 // Kernel design (CDNA4, wave64):
 //  * The work of a call is a list of tiles, one per (pair, layer, K/V); a
 //    tile is tile_bytes contiguous bytes on both sides.  A tile is cut into
-//    equal spans of whole 1 KiB rows and each span is one wavefront's work
-//    item: the wave issues all of its span's 1-KiB loads (64 lanes x 16
-//    bytes) before its first store, so each lane keeps up to 32 x 16 bytes
-//    in flight and the wave streams one contiguous span in and out.  A bulk
-//    launch cuts a tile into four spans (more when a span would pass 32
-//    rows), so the four wavefronts of a workgroup move one whole tile with
-//    equal shares: measured on MI355X, long per-wave spans beat
-//    interleaving the wavefronts over shared 4 KiB rows by 5-16% (128 KiB
-//    tiles: 32 KiB spans, 6.1-6.3 against 5.3-5.4 TB/s), and equal shares
-//    keep a workgroup from waiting on one long wave.  The kernel is built
-//    for SPAN rows, the power of two at or above the span; shorter spans
-//    and a tile's partial last row are predicated.  Launches with few items
-//    (a final stage) use 2 KiB spans so their tiles spread over more CUs.
+//    SPAN-KiB spans and each span is one wavefront's work item: the wave
+//    issues SPAN 1-KiB loads (64 lanes x 16 bytes, global_load_dwordx4)
+//    before its first store, so each lane keeps SPAN x 16 bytes in flight
+//    and the wave streams one contiguous span in and out.  SPAN is about a
+//    quarter of the tile, so the four wavefronts of a workgroup move one
+//    whole tile: measured on MI355X, long per-wave spans beat interleaving
+//    the wavefronts over shared 4 KiB rows by 5-16% (128 KiB tiles: 32 KiB
+//    spans, 6.1-6.3 against 5.3-5.4 TB/s).  Launches with few items (a
+//    final stage) use 2 KiB spans so their tiles spread over more CUs.
 //  * Wave items run pair-major (all spans of all layers of one block pair,
 //    then the next pair); one workgroup per four items unless the grid is
 //    capped, in which case resident workgroups walk the items.
@@ -70,7 +66,6 @@ struct CopyArgs {
     uint32_t planes;            // 2 * num_layers
     uint32_t pairs;             // pairs in this launch
     uint32_t spans_per_tile;
-    uint32_t span_bytes;        // bytes of one span: whole 1 KiB rows, at most SPAN of them
     uint32_t items;             // wave items: pairs * planes * spans_per_tile
     uint32_t lin_first;         // this launch's first pair within the whole call
     uint32_t lin_pairs;         // pairs in the whole call
@@ -125,11 +120,10 @@ __global__ void __launch_bounds__(kThreads) copy_tiles(const CopyArgs a)
 
         const __amdgpu_buffer_rsrc_t rs = tile_rsrc(s, a.tile_bytes);
         const __amdgpu_buffer_rsrc_t rd = tile_rsrc(d, a.tile_bytes);
-        const uint32_t base = span * a.span_bytes;
-        const uint32_t first = base + lane_off;
+        const uint32_t first = span * SPAN * kWaveRow + lane_off;
         u32x4 r[SPAN];
-        if (a.span_bytes == SPAN * kWaveRow && base + SPAN * kWaveRow <= a.tile_bytes) {
-            // Common case: a whole span of SPAN rows, no predication at all.
+        if ((span + 1) * SPAN * kWaveRow <= a.tile_bytes) {
+            // Common case: a whole span, no predication at all.
 #pragma unroll
             for (int u = 0; u < SPAN; ++u)
                 r[u] = buffer_load16(rs, first + u * kWaveRow);
@@ -137,16 +131,14 @@ __global__ void __launch_bounds__(kThreads) copy_tiles(const CopyArgs a)
             for (int u = 0; u < SPAN; ++u)
                 buffer_store16(rd, first + u * kWaveRow, r[u]);
         } else {
-            // A span shorter than SPAN rows, or the tile's last span: a lane
-            // predicate per 1 KiB row against the span's end.
-            const uint32_t end = min(base + a.span_bytes, a.tile_bytes);
+            // The tile's last span is short: a lane predicate per 1 KiB row.
 #pragma unroll
             for (int u = 0; u < SPAN; ++u)
-                if (first + u * kWaveRow < end)
+                if (first + u * kWaveRow < a.tile_bytes)
                     r[u] = buffer_load16(rs, first + u * kWaveRow);
 #pragma unroll
             for (int u = 0; u < SPAN; ++u)
-                if (first + u * kWaveRow < end)
+                if (first + u * kWaveRow < a.tile_bytes)
                     buffer_store16(rd, first + u * kWaveRow, r[u]);
         }
     }
@@ -164,28 +156,13 @@ uint32_t compute_units()
     return cus;
 }
 
-// Rows (1 KiB each, the last one possibly partial) of a tile.
-uint32_t tile_rows(uint32_t tile_bytes)
+// Span (in 1 KiB rows) for a bulk copy: the power of two nearest above a
+// quarter of the tile, between 2 and 32.
+int bulk_span(uint32_t tile_bytes)
 {
-    return static_cast<uint32_t>((static_cast<uint64_t>(tile_bytes) + kWaveRow - 1) / kWaveRow);
-}
-
-// Rows per span for a bulk copy: the tile cut into four equal spans, or
-// into more when a span would pass 32 rows (fewer when the tile has fewer
-// than four rows).
-uint32_t bulk_span_rows(uint32_t tile_bytes)
-{
-    const uint32_t rows = tile_rows(tile_bytes);
-    const uint32_t spans = std::max(std::min(4u, rows), (rows + 31) / 32);
-    return (rows + spans - 1) / spans;
-}
-
-// The kernel instance for spans of `rows` rows: the power of two at or
-// above it, between 2 and 32.
-int span_instance(uint32_t rows)
-{
+    const uint32_t quarter = (tile_bytes + 4 * kWaveRow - 1) / (4 * kWaveRow);
     int span = 2;
-    while (span < 32 && static_cast<uint32_t>(span) < rows)
+    while (span < 32 && static_cast<uint32_t>(span) < quarter)
         span *= 2;
     return span;
 }
@@ -230,17 +207,14 @@ int launch_copy(CopyArgs a, const int32_t *src_ids, const int32_t *dst_ids, int6
 {
     const int ids = ids_on_device ? kIdsDevice : (SRC == kPool && DST == kPool && ids16) ? kIds16 : kIds32;
     const int64_t inline_pairs = ids == kIds16 ? 2 * kInlinePairs : kInlinePairs;
-    const uint32_t rows = tile_rows(a.tile_bytes);
-    uint32_t span_rows = bulk_span_rows(a.tile_bytes);
-    uint32_t spt = (rows + span_rows - 1) / span_rows;
+    int span = bulk_span(a.tile_bytes);
+    uint32_t spt = (a.tile_bytes + span * kWaveRow - 1) / (span * kWaveRow);
     const uint64_t pairs_first_launch = std::min<int64_t>(n, ids_on_device ? n : inline_pairs);
     if (pairs_first_launch * 2ull * a.num_layers * spt < kBulkWaveItemsPerCU * compute_units()) {
-        span_rows = std::min(2u, rows);
-        spt = (rows + span_rows - 1) / span_rows;
+        span = 2;
+        spt = (a.tile_bytes + span * kWaveRow - 1) / (span * kWaveRow);
     }
-    const int span = span_instance(span_rows);
     a.spans_per_tile = spt;
-    a.span_bytes = span_rows * kWaveRow;
     const uint64_t items_per_pair = 2ull * a.num_layers * spt;
     uint64_t per_launch = std::min<uint64_t>(0x7fffffffull / items_per_pair,
                                              ids_on_device ? UINT64_MAX : static_cast<uint64_t>(inline_pairs));

@@ -127,14 +127,15 @@ class Migration:
 
 
 def run_scheduled(src: Pool, dst: Pool, src_table, dst_free_list, initial_len: int, appends,
-                  mig_stream, dec_stream, time_all: bool = False):
+                  mig_stream, dec_stream, time_all: bool = False, time_final: bool = False):
     """A migration whose decoding appends a known batch of tokens before each
     incremental stage (``appends`` is a list of device tensors laid out
     [L][K,V][n_tok][slot_bytes]); the stage after the last batch is final.
     Stage 0 is timed with events on the migration stream; the incremental
-    stages too when ``time_all``.  Returns (migration, downtime_us):
-    downtime is host wall time from the start of the final stage's planning
-    until the host sees it complete."""
+    stages too when ``time_all``, the final one when ``time_final`` (its
+    events then add their own host work to the downtime).  Returns
+    (migration, downtime_us): downtime is host wall time from the start of
+    the final stage's planning until the host sees it complete."""
     m = Migration(src, dst, src_table, dst_free_list, mig_stream)
     length = initial_len
     ready = torch.cuda.Event()
@@ -155,7 +156,7 @@ def run_scheduled(src: Pool, dst: Pool, src_table, dst_free_list, initial_len: i
             mig_stream.synchronize()
             ev.synchronize()
             t0 = time.perf_counter()
-            m.stage(length, final=True, time_it=False)
+            m.stage(length, final=True, time_it=time_final)
             mig_stream.synchronize()
             downtime_us = (time.perf_counter() - t0) * 1e6
         else:
@@ -171,14 +172,15 @@ def run_scheduled(src: Pool, dst: Pool, src_table, dst_free_list, initial_len: i
 
 def run_timed(src: Pool, dst: Pool, src_table, initial_len: int, dst_free_list, append_pool,
               mig_stream, dec_stream, step_ms: float = 20.0, last_stage_max_blocks: int = 1,
-              max_stages: int = 8, max_workgroups: int = 0):
+              max_stages: int = 8, max_workgroups: int = 0, time_final: bool = False):
     """A migration whose decoding speed is simulated: while a stage copies,
     decoding produces max(1, ceil(stage_time / step_ms)) tokens, which are
     written once the stage is over.  The next stage is final when at most
     ``last_stage_max_blocks`` blocks remain, or at ``max_stages``.
     ``append_pool`` is a device tensor [L][K,V][max_tokens][slot_bytes] the
     appended tokens are drawn from.  ``max_workgroups`` caps the copy grid
-    (0: uncapped).  Returns (migration, downtime_us)."""
+    (0: uncapped).  ``time_final`` times the final stage with events as
+    well.  Returns (migration, downtime_us)."""
     m = Migration(src, dst, src_table, dst_free_list, mig_stream, max_workgroups)
     length = initial_len
     max_tok = append_pool.shape[2]
@@ -203,7 +205,7 @@ def run_timed(src: Pool, dst: Pool, src_table, initial_len: int, dst_free_list, 
         if m.remaining_blocks(length) <= last_stage_max_blocks or len(m.stages) + 1 >= max_stages:
             ev.synchronize()
             t0 = time.perf_counter()
-            m.stage(length, final=True, time_it=False)
+            m.stage(length, final=True, time_it=time_final)
             mig_stream.synchronize()
             downtime_us = (time.perf_counter() - t0) * 1e6
             break
