@@ -340,6 +340,15 @@ def pin_multistage_replay(orc):
             assert length == cur
             events.append(("stage", length, lo, hi))
         dst_table, stages = orc.migrate(src, dst, table, free, events)
+        # every appended token's K and V bytes sit in its source slot
+        for ev in events:
+            if ev[0] == "append":
+                for j in range(ev[2].shape[2]):
+                    t = ev[1] + j
+                    cols = slice((t % bs) * slot, (t % bs + 1) * slot)
+                    for l in range(num_layers):
+                        assert np.array_equal(src.k[l][table[t // bs], cols], ev[2][l, 0, j])
+                        assert np.array_equal(src.v[l][table[t // bs], cols], ev[2][l, 1, j])
         assert len(dst_table) == nb
         assert np.array_equal(dst_table, free[:nb])
         assert np.array_equal(np.concatenate([s for s, _ in stages] + [np.zeros(0, np.int32)]),
@@ -669,6 +678,16 @@ def pin_xlayout_multistage_replay(orc):
                 cur += appended[k - 1]
             events.append(("stage", length, lo, hi))
         dst_table, _ = orc.migrate(src, dst, table, free, events, layouts=(sl, dl, heads, dim, e))
+        # every appended token sits in its source slot, in the source's layouts
+        for ev in events:
+            if ev[0] == "append":
+                for j in range(ev[2].shape[2]):
+                    t = ev[1] + j
+                    for l in range(num_layers):
+                        for kv, arr in ((0, src.k[l]), (1, src.v[l])):
+                            got = _logical(arr[table[t // bs]], sl[kv], bs, heads, dim, e)[t % bs]
+                            want = np.ascontiguousarray(ev[2][l, kv, j]).view(_UINT[e]).reshape(heads, dim)
+                            assert np.array_equal(got, want), (sl, l, kv, t)
         assert np.array_equal(dst_table, free[:nb])
         for l in range(num_layers):
             for kv in range(2):

@@ -1,7 +1,7 @@
 """Every plausible single mistake planted in a copy of the CPU oracle must
 fail at least one pin: evidence that the pins can tell a wrong oracle from a
 right one.  The mistakes are planted in temporary copies of the oracle's C
-source; the oracle itself is never changed."""
+source and of its Python replay code; the oracle itself is never changed."""
 import os
 import subprocess
 import sys
@@ -72,6 +72,21 @@ MUTANTS = [
      "const uint8_t *s = staging + ((i * 2 + kv) * num_layers + l) * tile_bytes;", 0),
 ]
 
+# Mistakes in the Python side of the oracle (the multi-stage replay and the
+# stage schedule of Llumnix §4.2), planted in a copy of oracle/__init__.py.
+PY_MUTANTS = [
+    ("replay_free_list_not_advanced", "free = free[len(md):]", "free = free"),
+    ("replay_appends_dropped", "self.write_tokens(src, src_table, ev[1], ev[2])", "pass"),
+    ("replay_table_from_sources", "dst_table.extend(int(x) for x in md)", "dst_table.extend(int(x) for x in ms)"),
+    ("schedule_final_whole_blocks", "end = length if final else (length // block_size) * block_size",
+     "end = (length // block_size) * block_size"),
+    ("schedule_restarts_each_stage", "        copied = end", "        copied = 0"),
+    ("replay_layout_appends_dropped",
+     "self.write_tokens_layout(src, layouts[0], src_table, ev[1], ev[2], *layouts[2:])", "pass"),
+    ("replay_layout_copy_unconverted", "self.copy_layout(src, layouts[0], dst, layouts[1], ms, md, *layouts[2:])",
+     "self.copy(src, dst, ms, md)"),
+]
+
 RUNNER = r"""
 import sys
 sys.path[:0] = [sys.argv[1], sys.argv[2]]
@@ -122,3 +137,22 @@ def test_every_planted_mistake_fails_a_pin():
             caught = {name: f.result() for name, f in futures.items()}
     missed = [name for name, failed in caught.items() if not failed]
     assert not missed, f"mutants no pin catches: {missed}"
+
+
+def test_every_planted_replay_mistake_fails_a_pin():
+    py_src = open(os.path.join(os.path.dirname(oracle.SOURCE), "__init__.py")).read()
+    tests_dir = os.path.dirname(os.path.abspath(__file__))
+    lib = oracle.LIBRARY if os.path.exists(oracle.LIBRARY) else oracle.build()   # the unchanged C oracle
+    with tempfile.TemporaryDirectory() as tmp:
+        roots = {}
+        for name, old, new in PY_MUTANTS:
+            root = os.path.join(tmp, name)
+            os.makedirs(os.path.join(root, "oracle"))
+            with open(os.path.join(root, "oracle", "__init__.py"), "w") as f:
+                f.write(_mutate(py_src, old, new, 0))
+            roots[name] = root
+        with ThreadPoolExecutor(max_workers=6) as pool:
+            futures = {name: pool.submit(_run_pins, root, tests_dir, lib) for name, root in roots.items()}
+            caught = {name: f.result() for name, f in futures.items()}
+    missed = [name for name, failed in caught.items() if not failed]
+    assert not missed, f"replay mutants no pin catches: {missed}"
