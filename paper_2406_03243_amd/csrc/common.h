@@ -14,6 +14,10 @@ namespace {
 constexpr int kThreads = 256;                 // 4 wavefronts of 64 lanes
 constexpr uint32_t kRowBytes = kThreads * 16; // one 16-byte word per lane of a workgroup
 constexpr int kInlinePairs = 256;             // ids carried in the kernel arguments per launch
+// Grid cap of the grid-stride kernels (copy, conversion, token writes): a
+// dispatch counts its work-items in 32 bits, and past a few million
+// workgroups more of them would only wait in the queue.
+constexpr uint32_t kMaxGridWorkgroups = 1u << 22;
 
 // Where a launch finds its block ids.
 enum Ids {

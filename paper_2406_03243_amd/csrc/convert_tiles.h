@@ -310,7 +310,7 @@ int launch_convert(ConvertArgs a, const int32_t *src_ids, const int32_t *dst_ids
             std::memcpy(a.ids + kInlinePairs, dst_ids + first, m * sizeof(int32_t));
         }
         void *args[] = {&a};
-        uint32_t grid = (a.units + kConvertWaves - 1) / kConvertWaves;
+        uint32_t grid = std::min((a.units + kConvertWaves - 1) / kConvertWaves, kMaxGridWorkgroups);
         if (max_workgroups > 0)
             grid = std::min(grid, max_workgroups);
         hipError_t e = launch_kernel(fn, dim3(grid), dim3(kConvertWaves * 64), args, stream, ev, k, launches);

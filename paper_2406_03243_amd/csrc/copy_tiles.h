@@ -242,7 +242,7 @@ int launch_copy(CopyArgs a, const int32_t *src_ids, const int32_t *dst_ids, int6
                 std::memcpy(a.ids + kInlinePairs, dst_ids + first, m * sizeof(int32_t));
         }
         void *args[] = {&a};
-        uint32_t grid = (a.items + kThreads / 64 - 1) / (kThreads / 64);
+        uint32_t grid = std::min((a.items + kThreads / 64 - 1) / (kThreads / 64), kMaxGridWorkgroups);
         if (max_workgroups > 0)
             grid = std::min(grid, max_workgroups);
         hipError_t e = launch_kernel(fn, dim3(grid), dim3(kThreads), args, stream, ev, k, launches);

@@ -808,7 +808,7 @@ int llmig_write_tokens(const llmig_pool *pool, const int32_t *table, int64_t tab
         void *args[] = {&a};
         const uint32_t items = a.tokens * 2u * a.num_layers;
         hipError_t e = hipLaunchKernel(reinterpret_cast<const void *>(&write_token_slots),
-                                       dim3(items), dim3(kThreads), args, 0,
+                                       dim3(std::min(items, kMaxGridWorkgroups)), dim3(kThreads), args, 0,
                                        static_cast<hipStream_t>(stream));
         if (e != hipSuccess)
             return hip_error(e);

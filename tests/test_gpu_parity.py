@@ -471,3 +471,47 @@ def test_largest_tiles():
     k2, v2 = harness.alloc_layers(wl.PoolShape(1, 1, 1, 1, dim + 8, "fp16"))
     with pytest.raises(LlmigError):                    # 2^31 bytes: one byte past the limit
         Pool(k2, v2)
+
+
+def test_grids_past_the_workgroup_cap():
+    """Launches whose one-workgroup-per-item grid would pass the grid cap
+    (2^22 workgroups) run on the capped grid, each workgroup walking several
+    items: a 9-million-pair stage of 16-byte tiles with device ids, and a
+    131072-token write of 128 planes through 256 blocks of 512 slots."""
+    say("grid cap: 9e6 pairs of 16-byte tiles")
+    shape = wl.PoolShape(1, 9_500_000, 1, 1, 8, "fp16")
+    k, v = harness.alloc_layers(shape)
+    dk, dv = harness.alloc_layers(shape)
+    g = torch.Generator(device="cuda")
+    g.manual_seed(9500)
+    for t in k + v + dk + dv:
+        t.view(torch.int16).random_(-32768, 32767, generator=g)
+    src, dst = Pool(k, v), Pool(dk, dv)
+    n = 9_000_000
+    ms = torch.randperm(shape.num_blocks, device="cuda", generator=g)[:n].to(torch.int32)
+    md = torch.randperm(shape.num_blocks, device="cuda", generator=g)[:n].to(torch.int32)
+    assert n * 2 // 4 > (1 << 22)                      # the uncapped grid would be larger
+    before = [t.clone() for t in dk + dv]
+    llmig.llmig_stage(src, dst, ms, md)
+    torch.cuda.synchronize()
+    mask = torch.ones(shape.num_blocks, dtype=torch.bool, device="cuda")
+    mask[md.long()] = False
+    for s_t, d_t, b_t in zip(k + v, dk + dv, before):     # compared as bits: the patterns include NaNs
+        s_t, d_t, b_t = s_t.view(torch.int16), d_t.view(torch.int16), b_t.view(torch.int16)
+        assert torch.equal(d_t[md.long()], s_t[ms.long()])
+        assert torch.equal(d_t[mask], b_t[mask])
+    del before, k, v, dk, dv, src, dst
+    torch.cuda.empty_cache()
+
+    say("grid cap: 131072-token write")
+    shape = wl.PoolShape(64, 300, 512, 1, 8, "fp16")
+    pool = make_pool(shape, 9501, wl.SRC_VALUES, random_bytes=True)
+    table = wl.stream(9501, wl.EXTRA).choice(300, 256, replace=False).astype(np.int32)
+    n_tok = 256 * 512
+    data = wl.random_bytes(9501, wl.APPEND_VALUES, shape.num_layers * 2 * n_tok * pool.slot_bytes)
+    assert n_tok * 2 * shape.num_layers > (1 << 22)
+    want = host_image(pool)
+    llmig.llmig_write_tokens(pool, table, 0, torch.from_numpy(data).cuda())
+    torch.cuda.synchronize()
+    oracle.default().write_tokens(want, table, 0, data.reshape(shape.num_layers, 2, n_tok, pool.slot_bytes))
+    assert_same(host_image(pool), want, "pool after the write")
