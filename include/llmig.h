@@ -29,7 +29,9 @@
  *
  * Error convention: every entry point returns LLMIG_OK (0) or a negative
  * code.  All argument checks run before anything is enqueued, so a call that
- * fails has no effect.  Nothing throws or aborts across this interface.
+ * fails a check has no effect; only LLMIG_EHIP, a runtime error during a
+ * call's launches, may leave part of the call enqueued.  Nothing throws or
+ * aborts across this interface.
  *
  * Threads and streams: llmig_plan is pure.  The other calls only enqueue on
  * the stream they are given and may be called from several threads on
