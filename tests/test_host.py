@@ -5,6 +5,7 @@ enqueueing calls fail before touching the GPU."""
 import ctypes
 import os
 import re
+import subprocess
 
 import numpy as np
 import pytest
@@ -180,3 +181,43 @@ def test_workload_generators_are_seeded_and_shaped():
     ref = torch.from_numpy(g.uniform(-1.0, 1.0, size=10000).astype(np.float32)).to(torch.bfloat16)
     assert torch.equal(ref.view(torch.int16),
                        torch.from_numpy(wl.values16(5, wl.SRC_VALUES, 10000, "bf16").view(np.int16)))
+
+
+C_CLIENT = r"""
+#include <stdio.h>
+#include "llmig.h"
+
+int main(void)
+{
+    /* a request of 40 tokens in blocks of 16: three logical blocks */
+    const int32_t table[3] = {7, 2, 9};
+    const int32_t free_list[4] = {11, 12, 13, 14};
+    int32_t out_src[4], out_dst[4];
+    int64_t n = -1;
+    llmig_pool_desc desc = {0};
+    llmig_pool *pool = NULL;
+    int rc = llmig_plan(table, 3, free_list, 4, 40, 16, 40, 16, out_src, out_dst, 4, &n);
+    if (rc != LLMIG_OK || n != 2 || out_src[0] != 2 || out_src[1] != 9 || out_dst[0] != 11 || out_dst[1] != 12)
+        return 1;
+    if (llmig_plan(table, 3, free_list, 1, 40, 0, 40, 16, out_src, out_dst, 4, &n) != LLMIG_ENOSPC || n != 0)
+        return 2;
+    if (llmig_pool_create(&desc, &pool) != LLMIG_EINVAL || pool != NULL)
+        return 3;
+    printf("%s\n", llmig_strerror(LLMIG_ERANGE));
+    return 0;
+}
+"""
+
+
+def test_header_is_plain_c(tmp_path):
+    """llmig.h compiles as C99 with every warning an error, and a C program
+    linked against the library plans a stage through it (no GPU needed)."""
+    src = tmp_path / "client.c"
+    src.write_text(C_CLIENT)
+    exe = tmp_path / "client"
+    lib_dir = os.path.dirname(llmig.LIBRARY)
+    subprocess.run(["gcc", "-std=c99", "-Wall", "-Wextra", "-Werror", "-pedantic", "-I", os.path.join(ROOT, "include"),
+                    str(src), "-o", str(exe), "-L", lib_dir, "-lllmig", "-Wl,-rpath," + lib_dir], check=True)
+    res = subprocess.run([str(exe)], capture_output=True, text=True, timeout=60)
+    assert res.returncode == 0, (res.returncode, res.stderr)
+    assert res.stdout.strip() == "block id out of range"
