@@ -19,7 +19,7 @@ from paper_2406_03243_amd import workloads as wl
 pytestmark = pytest.mark.gpu
 
 if torch.cuda.is_available():
-    from paper_2406_03243_amd import migrate
+    from paper_2406_03243_amd import llmig, migrate
     from paper_2406_03243_amd.llmig import Pool
 
 NHD, HND, HCNX, HDN = 0, 1, 2, 3
@@ -104,3 +104,51 @@ def test_random_migration(seed):
         torch.cuda.synchronize()
         assert np.array_equal(np.asarray(m2.dst_table, np.int32), want_table)
         assert host_image(dst2).equals(gd), "capped grid differs"
+
+
+@pytest.mark.parametrize("seed", range(60))
+def test_random_block_fusion(seed):
+    """Block fusion (§5) on random cases: pack a random list of source blocks
+    (repeats allowed) into device or pinned staging, unpack it into distinct
+    destination blocks, converting between layouts where they differ; ids
+    from the host or the device."""
+    g = wl.stream(20_000 + seed, wl.EXTRA)
+    layers, bs, heads, dim, dtype, (sl, dl), _, _, _ = draw_case(20_000 + seed)
+    n = int(g.integers(1, 80))
+    nbs, nbd = int(g.integers(1, 100)), n + int(g.integers(0, 40))
+    where = str(g.choice(["device", "pinned"]))
+    dev_ids = bool(g.random() < 0.5)
+    print("[case] random fusion", seed, dict(layers=layers, bs=bs, heads=heads, dim=dim, src=sl, dst=dl, n=n,
+                                               staging=where, device_ids=dev_ids), flush=True)
+    sk, sv = harness.alloc_layers(wl.PoolShape(layers, nbs, bs, heads, dim, dtype))
+    dk, dv = harness.alloc_layers(wl.PoolShape(layers, nbd, bs, heads, dim, dtype))
+    harness.fill_bytes_from_host(sk + sv, wl.random_bytes(seed, wl.SRC_VALUES, sum(t.numel() * 2 for t in sk + sv)))
+    harness.fill_bytes_from_host(dk + dv, wl.random_bytes(seed, wl.DST_VALUES, sum(t.numel() * 2 for t in dk + dv)))
+    src, dst = Pool(sk, sv, layouts=sl), Pool(dk, dv, layouts=dl)
+    blocks = g.integers(0, nbs, n).astype(np.int32)            # repeats allowed when packing
+    into = g.permutation(nbd)[:n].astype(np.int32)
+    nbytes = n * layers * 2 * src.tile_bytes
+    if where == "device":
+        staging = torch.empty(nbytes + 48, dtype=torch.uint8, device="cuda")
+    else:
+        staging = torch.empty(nbytes + 48, dtype=torch.uint8, pin_memory=True)
+    staging.fill_(0x5C)
+    torch.cuda.synchronize()
+    hs, hd = host_image(src), host_image(dst)
+    ids_b = torch.from_numpy(blocks).cuda() if dev_ids else blocks
+    ids_i = torch.from_numpy(into).cuda() if dev_ids else into
+    llmig.llmig_pack(src, ids_b, staging)
+    torch.cuda.synchronize()
+    got = staging.cpu().numpy()
+    want = oracle.default().pack(hs, blocks)
+    assert np.array_equal(got[:nbytes], want)
+    assert (got[nbytes:] == 0x5C).all()
+    if sl == dl:
+        llmig.llmig_unpack(dst, ids_i, staging)
+        oracle.default().unpack(hd, into, want)
+    else:
+        llmig.llmig_unpack_layout(dst, ids_i, staging, sl)
+        oracle.default().unpack_layout(hd, dl, into, want, sl, heads, dim, 2)
+    torch.cuda.synchronize()
+    assert host_image(dst).equals(hd), "destination differs from the oracle"
+    assert host_image(src).equals(hs), "source changed"
