@@ -83,6 +83,27 @@ def test_decode_attention_matches_oracle(case):
     run_case(*case, seed=500 + sum(case[6]) % 97)
 
 
+def random_case(seed):
+    g = wl.stream(seed, wl.LENGTHS)
+    bs = int(g.choice([1, 2, 4, 8, 16, 32]))
+    batch = int(g.integers(1, 9))
+    ctx = [int(x) for x in g.integers(0, 1500, batch)]
+    if g.random() < 0.2:
+        ctx[int(g.integers(0, batch))] = 0
+    blocks = max(1, max(-(-c // bs) for c in ctx)) + int(g.integers(0, 20))
+    return (int(g.integers(1, 4)), blocks, bs, int(g.integers(1, 5)), int(g.choice([64, 128])),
+            int(g.choice([1, 2, 4, 8, 16])), ctx, str(g.choice(["fp16", "bf16"])))
+
+
+@pytest.mark.parametrize("seed", range(30))
+def test_decode_attention_random(seed):
+    """30 seeded random shapes: layers, block size 1-32, KV heads, head dim,
+    group size, batch, context lengths (zero included) and type."""
+    case = random_case(30_000 + seed)
+    say("decode attention random", seed, case)
+    run_case(*case, seed=30_000 + seed)
+
+
 def test_decode_attention_rejects_unsupported():
     say("decode attention errors")
     shape = wl.PoolShape(1, 20, 16, 2, 96, "fp16")
