@@ -45,7 +45,7 @@
 
 /*
  * Plan one migration stage (Llumnix §4.2: before each stage the source asks
- * the destination to pre-allocate "the number of blocks to migrate"; stage k
+ * the destination to pre-allocate as many blocks as the stage moves; stage k
  * copies the KV produced since stage k-1).
  *
  * The stage covers tokens [from_tok, to_tok) of a request whose first `len`
