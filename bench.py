@@ -205,6 +205,22 @@ def main():
         mf, _ = migrate.run_scheduled(src, dst, table, free, initial, appends, mig, dec, time_final=True)
         final_gpu.append(mf.stages[-1].gpu_us)
 
+    # The same launch on contiguous tiles (block i of every layer tensor to
+    # block i, as many blocks as stage 1), outside the timed region: what
+    # the scattering of a real block table costs the copy.
+    from paper_2406_03243_amd.llmig import llmig_stage
+    ident = np.arange(s1_blocks, dtype=np.int32)
+    cont_us = []
+    for r in range(13):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(mig)
+        llmig_stage(src, dst, ident, ident, stream=mig)
+        e1.record(mig)
+        e1.synchronize()
+        if r >= 3:
+            cont_us.append(e0.elapsed_time(e1) * 1e3)
+    cont_gbs = stage_bytes(s1_blocks, shape, src.tile_bytes) / (statistics.median(cont_us) * 1e-6) / 1e9
+
     stages = []
     for i, rec in enumerate(m0.stages):
         us = [m.stages[i].gpu_us for m, _ in runs if m.stages[i].gpu_us > 0]
@@ -243,7 +259,9 @@ def main():
                      "traffic": recorded_traffic(kernel_name),
                      "kernel": kernel_name,
                      "launches_per_stage": launches, "bytes_per_launch": int(per_launch_bytes),
-                     "avg_launch_us": round(per_launch_us, 2)},
+                     "avg_launch_us": round(per_launch_us, 2),
+                     "contiguous_tiles_GBps": round(cont_gbs, 1),
+                     "scattered_vs_contiguous": round(achieved / cont_gbs, 3)},
         "stages": stages,
         "streams_overlap": overlap,
         # the paper's own figures, from another machine and transport: context only
