@@ -227,12 +227,13 @@ int llmig_write_tokens(const llmig_pool *pool, const int32_t *table, int64_t tab
 /* ---------------------------------------------------------------------------
  * Migration coordinator: the handshake of §4.2 as a host state machine.
  *
- * Before each stage the source asks the destination to pre-allocate the
- * blocks the stage migrates; the destination reserves them or refuses, and a
- * refusal aborts the migration.  After each stage the source checks whether
- * the request finished or was preempted, and aborts (releasing the reserved
- * blocks) if so; either side aborts when the other fails.  After the final
- * stage the source releases its blocks and the destination commits.
+ *   each stage  reserves its destination blocks first (a refusal means
+ *               abort), then copies;
+ *   between     a request that has meanwhile finished or been preempted
+ *   stages      is aborted, which hands every reserved block back;
+ *   failures    of either side also end in an abort;
+ *   the end     after the final stage, a commit: the destination takes the
+ *               request over and the source may free its blocks.
  *
  * A llmig_migration holds the request's progress: tokens copied so far, the
  * destination blocks reserved so far (in logical order), the stage count and

@@ -44,9 +44,8 @@
 #define ORACLE_ERANGE (-3)
 
 /*
- * Plan one migration stage (Llumnix §4.2: before each stage the source asks
- * the destination to pre-allocate as many blocks as the stage moves; stage k
- * copies the KV produced since stage k-1).
+ * Plan one migration stage (Llumnix §4.2: a stage first reserves its
+ * destination blocks, then copies the KV produced since the stage before).
  *
  * The stage covers tokens [from_tok, to_tok) of a request whose first `len`
  * tokens are resident in the source pool.  Logical block j holds tokens
