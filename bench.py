@@ -115,7 +115,7 @@ def main():
     ap.add_argument("--sections", default="downtime,batched,load,xlayout",
                     help="extra workloads after the main one (comma list of downtime, batched, load, xlayout;"
                          " empty for none)")
-    ap.add_argument("--downtime-reps", type=int, default=7)
+    ap.add_argument("--downtime-reps", type=int, default=20)
     ap.add_argument("--no-gc-freeze", action="store_true", help="leave set-up objects to the collector")
     ap.add_argument("--calibration-copy", action="store_true",
                     help="end with two plain 1 GiB device-to-device copies (hardware counter calibration)")
@@ -271,7 +271,9 @@ def main():
                                    "network, KV sent with Gloo through CPU buffers; LLaMA-7B and LLaMA-30B",
                           "source": "Llumnix section 6.2"},
         "final_stage_downtime_us": {"median": round(statistics.median(downtimes), 1),
-                                    "min": round(min(downtimes), 1), "max": round(max(downtimes), 1)},
+                                    "min": round(min(downtimes), 1), "max": round(max(downtimes), 1),
+                                    "p10": round(percentile(downtimes, 10), 2),
+                                    "p90": round(percentile(downtimes, 90), 2), "n": len(downtimes)},
         "final_stage_gpu_us": spread(final_gpu),
     }
 
@@ -423,8 +425,11 @@ def downtime_sweep(reps):
             "final_blocks": res[0][0].stages[-1].blocks,
             "downtime_us_median": round(statistics.median(dt for _, dt in res), 1),
             "downtime_us_min": round(min(dt for _, dt in res), 1),
+            "downtime_us": spread([dt for _, dt in res]),
             "final_stage_gpu_us_median": round(statistics.median(final_gpu), 1),
+            "final_stage_gpu_us": spread(final_gpu),
             "blocking_copy_downtime_us_median": round(statistics.median(blocking), 1),
+            "blocking_copy_downtime_us": spread(blocking),
         }
     su.close()
     return out
