@@ -515,3 +515,20 @@ def test_grids_past_the_workgroup_cap():
     torch.cuda.synchronize()
     oracle.default().write_tokens(want, table, 0, data.reshape(shape.num_layers, 2, n_tok, pool.slot_bytes))
     assert_same(host_image(pool), want, "pool after the write")
+
+
+@pytest.mark.parametrize("bs,lo,n_tok", [(1, 0, 700), (4, 3, 1500), (16, 17, 5000)])
+def test_write_tokens_across_launches(bs, lo, n_tok):
+    """The decode stand-in over more blocks than one launch carries (256):
+    several launches, a first block entered mid-way, a partial last one."""
+    say("write tokens across launches", bs, lo, n_tok)
+    nb = (lo + n_tok + bs - 1) // bs
+    shape = wl.PoolShape(2, nb + 40, bs, 2, 64, "bf16")
+    pool = make_pool(shape, 9600 + bs, wl.SRC_VALUES, random_bytes=True)
+    table = wl.stream(9600 + bs, wl.EXTRA).choice(nb + 40, nb, replace=False).astype(np.int32)
+    data = wl.random_bytes(9600 + bs, wl.APPEND_VALUES, 2 * 2 * n_tok * pool.slot_bytes)
+    want = host_image(pool)
+    llmig.llmig_write_tokens(pool, table, lo, torch.from_numpy(data).cuda())
+    torch.cuda.synchronize()
+    oracle.default().write_tokens(want, table, lo, data.reshape(2, 2, n_tok, pool.slot_bytes))
+    assert_same(host_image(pool), want, "pool after the write")
