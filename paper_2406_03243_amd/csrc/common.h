@@ -92,9 +92,11 @@ __device__ __forceinline__ void store16(uint8_t *p, u32x4 v)
 
 // Raw buffer accesses (the migration copy): a resource over one tile, and
 // 16-byte loads and stores with explicit cache-policy bits.  On gfx950 the
-// policy bits are sc0 = 1, nt = 2, sc1 = 16.  Loads stream (nt); stores
-// also carry sc1, measured 0.5-1.3% faster on the LLaMA-7B stage than nt
-// alone (plain or sc0 stores were 2-10% slower).
+// policy bits are sc0 = 1, nt = 2, sc1 = 16 (sc1 alone selects device
+// scope).  Loads stream (nt); stores also carry sc1, measured 0.5-1.3%
+// faster on the LLaMA-7B stage than nt alone (plain or sc0 stores were
+// 2-10% slower).  An access whose offset lies past the resource's
+// num_records is out of range: a load returns zeros and a store is dropped.
 constexpr int kBufferWord3 = 0x00020000;     // descriptor word 3 for raw 32-bit accesses on gfx9
 constexpr int kStreamLoad = 2;               // nt
 constexpr int kStreamStore = 16 | 2;         // sc1 nt

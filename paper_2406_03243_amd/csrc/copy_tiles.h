@@ -11,14 +11,25 @@
 //  * The work of a call is a list of tiles, one per (pair, layer, K/V); a
 //    tile is tile_bytes contiguous bytes on both sides.  A tile is cut into
 //    SPAN-KiB spans and each span is one wavefront's work item: the wave
-//    issues SPAN 1-KiB loads (64 lanes x 16 bytes, global_load_dwordx4)
-//    before its first store, so each lane keeps SPAN x 16 bytes in flight
-//    and the wave streams one contiguous span in and out.  SPAN is about a
-//    quarter of the tile, so the four wavefronts of a workgroup move one
-//    whole tile: measured on MI355X, long per-wave spans beat interleaving
-//    the wavefronts over shared 4 KiB rows by 5-16% (128 KiB tiles: 32 KiB
-//    spans, 6.1-6.3 against 5.3-5.4 TB/s).  Launches with few items (a
-//    final stage) use 2 KiB spans so their tiles spread over more CUs.
+//    issues SPAN 1-KiB loads (64 lanes x 16 bytes) before its first store,
+//    so each lane keeps SPAN x 16 bytes in flight and the wave streams one
+//    contiguous span in and out.  SPAN is about a quarter of the tile, so
+//    the four wavefronts of a workgroup move one whole tile: measured on
+//    MI355X, long per-wave spans beat interleaving the wavefronts over
+//    shared 4 KiB rows by 5-16% (128 KiB tiles: 32 KiB spans, 6.1-6.3
+//    against 5.3-5.4 TB/s).  Launches with few items (a final stage) use
+//    2 KiB spans so their tiles spread over more CUs.
+//  * Every span runs the same unpredicated sequence of SPAN loads and SPAN
+//    stores.  A row of the span that lies past the end of the tile (the
+//    last span of a tile that is not a whole number of spans, such as the
+//    4 KiB tail of a 52 KiB tile cut into 16 KiB spans) gets an offset past
+//    the buffer resource's range, so the hardware's range check returns
+//    zeros for its load and drops its store.  Predicating those rows on
+//    the lane mask instead makes the compiler wait for every earlier memory
+//    operation before each store of the span (it cannot count them across
+//    the branches), which serialised the tail's stores: 52 KiB tiles moved
+//    at 0.62-0.67 of HBM peak that way and at 0.72-0.75 this way, in one
+//    process, alternating (128 and 32 KiB tiles gained about 1%).
 //  * Wave items run pair-major (all spans of all layers of one block pair,
 //    then the next pair); one workgroup per four items unless the grid is
 //    capped, in which case resident workgroups walk the items.
@@ -37,8 +48,9 @@
 //    has no arithmetic.
 //  * Loads and stores are raw buffer accesses over one tile with explicit
 //    cache policy: non-temporal loads, and stores that are non-temporal
-//    with system scope (sc1).  Every byte is touched once, and streaming it
-//    past the caches leaves them to the decode work beside the migration.
+//    with the sc1 scope bit (device scope on gfx950).  Every byte is touched
+//    once, and streaming it past the caches leaves them to the decode work
+//    beside the migration.
 #pragma once
 
 #include <algorithm>
@@ -73,6 +85,19 @@ struct CopyArgs {
 };
 
 constexpr uint32_t kWaveRow = 64 * 16;         // one wavefront load: 1 KiB
+
+// Buffer offset of the row starting at byte o of a tile of `bytes` bytes:
+// o itself, or kOutOfRange when the row lies past the tile.  Tiles are at
+// most 2^31 - 1 bytes, so kOutOfRange plus a lane's offset is always past
+// the resource's range: the load returns zeros and the store is dropped.
+// A row that is partly inside the tile (a tile that is not a whole number
+// of KiB) is cut per lane by the same check.
+constexpr uint32_t kOutOfRange = 0x80000000u;
+
+__device__ __forceinline__ uint32_t row_offset(uint32_t o, uint32_t bytes)
+{
+    return o < bytes ? o : kOutOfRange;
+}
 
 template <int IDS>
 __device__ __forceinline__ uint32_t src_id(const CopyArgs &a, uint32_t i)
@@ -120,27 +145,14 @@ __global__ void __launch_bounds__(kThreads) copy_tiles(const CopyArgs a)
 
         const __amdgpu_buffer_rsrc_t rs = tile_rsrc(s, a.tile_bytes);
         const __amdgpu_buffer_rsrc_t rd = tile_rsrc(d, a.tile_bytes);
-        const uint32_t first = span * SPAN * kWaveRow + lane_off;
+        const uint32_t first = span * SPAN * kWaveRow;
         u32x4 r[SPAN];
-        if ((span + 1) * SPAN * kWaveRow <= a.tile_bytes) {
-            // Common case: a whole span, no predication at all.
 #pragma unroll
-            for (int u = 0; u < SPAN; ++u)
-                r[u] = buffer_load16(rs, first + u * kWaveRow);
+        for (int u = 0; u < SPAN; ++u)
+            r[u] = buffer_load16(rs, row_offset(first + u * kWaveRow, a.tile_bytes) + lane_off);
 #pragma unroll
-            for (int u = 0; u < SPAN; ++u)
-                buffer_store16(rd, first + u * kWaveRow, r[u]);
-        } else {
-            // The tile's last span is short: a lane predicate per 1 KiB row.
-#pragma unroll
-            for (int u = 0; u < SPAN; ++u)
-                if (first + u * kWaveRow < a.tile_bytes)
-                    r[u] = buffer_load16(rs, first + u * kWaveRow);
-#pragma unroll
-            for (int u = 0; u < SPAN; ++u)
-                if (first + u * kWaveRow < a.tile_bytes)
-                    buffer_store16(rd, first + u * kWaveRow, r[u]);
-        }
+        for (int u = 0; u < SPAN; ++u)
+            buffer_store16(rd, row_offset(first + u * kWaveRow, a.tile_bytes) + lane_off, r[u]);
     }
 }
 
