@@ -58,6 +58,8 @@ extern "C" {
                              pre-allocation fails and the migration aborts) */
 #define LLMIG_ERANGE (-3) /* a block id outside [0, num_blocks) */
 #define LLMIG_EHIP (-4)   /* the HIP runtime reported an error: see llmig_last_hip_error */
+#define LLMIG_ESCRATCH (-5) /* the call needs more than the library's static scratch array
+                               (LLMIG_DECODE_SCRATCH_BYTES) holds; nothing was enqueued */
 
 /* Intra-tile layouts.  A (layer, K or V, block) tile holds block_size
  * tokens x num_kv_heads heads x head_dim dims; x = 16 / elem_bytes dims make
@@ -355,6 +357,31 @@ int llmig_decode_attention(const llmig_pool *pool, int32_t dtype, const void *q,
                            int32_t q_heads, const int32_t *tables, int32_t table_stride,
                            const int32_t *ctx_lens, float scale, void *workspace,
                            int64_t workspace_bytes, float *out, void *stream);
+
+/* ---------------------------------------------------------------------------
+ * For callers that cannot allocate device memory: code being captured into a
+ * HIP graph, serving loops that must not call hipMalloc, harnesses that
+ * forbid it.
+ *
+ * llmig_decode_attention_noalloc is llmig_decode_attention without the
+ * workspace: the partial results go to one static device array of
+ * LLMIG_DECODE_SCRATCH_BYTES (32 MiB) that every GPU the library runs on
+ * holds until the process ends.  The call allocates nothing (no hipMalloc,
+ * hipFree or allocating library routine); the array's device address is
+ * looked up when the first pool is registered on a GPU (or, failing that,
+ * at this call's first use there).  Every call on one GPU shares that GPU's
+ * array, which keeps the last call's contents: calls that overlap on one
+ * GPU (two streams, two threads) race and give wrong results, so the caller
+ * serialises them.  Nothing in the array has to start at zero: a call writes
+ * every entry it reads.  A call whose partial results need more than the
+ * array (the size llmig_decode_attention_workspace gives for the same
+ * lengths) returns LLMIG_ESCRATCH and enqueues nothing.  Other arguments,
+ * results and errors as llmig_decode_attention.
+ * ------------------------------------------------------------------------- */
+#define LLMIG_DECODE_SCRATCH_BYTES (32u << 20)
+int llmig_decode_attention_noalloc(const llmig_pool *pool, int32_t dtype, const void *q, int32_t batch,
+                                   int32_t q_heads, const int32_t *tables, int32_t table_stride,
+                                   const int32_t *ctx_lens, float scale, float *out, void *stream);
 
 /* Static description of a code; never NULL. */
 const char *llmig_strerror(int code);

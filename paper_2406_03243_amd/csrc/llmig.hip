@@ -17,6 +17,7 @@
 #include <cstdint>
 #include <cstring>
 #include <memory>
+#include <mutex>
 #include <new>
 #include <utility>
 #include <vector>
@@ -47,6 +48,14 @@ struct llmig_migration {
     std::vector<int32_t> plan_src;    // per-stage scratch, reused
     std::vector<int32_t> plan_dst;
 };
+
+// Partial results of llmig_decode_attention_noalloc (the entry point for
+// callers that cannot allocate): one static array, of which every GPU the
+// library runs on holds its own copy until the process ends.  Host code
+// never uses the array's name as an address: it reaches each device's copy
+// through the address hipGetSymbolAddress gives with that device current
+// (scratch_pointer below).
+__device__ __align__(256) uint8_t scratch[LLMIG_DECODE_SCRATCH_BYTES];
 
 namespace {
 
@@ -160,6 +169,30 @@ bool on_current_device(const llmig_pool *pool)
 {
     int d = -1;
     return hipGetDevice(&d) == hipSuccess && d == pool->device;
+}
+
+// Device address of `scratch` on each device, looked up once per device
+// with that device current (at its first llmig_pool_create, else at the
+// first llmig_decode_attention_noalloc there) and kept for the process.
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mutex;
+void *g_scratch_ptr[kMaxDevices] = {};
+
+// The current device's scratch address, looked up on first use.
+int scratch_pointer(int device, void **out)
+{
+    if (device < 0 || device >= kMaxDevices)
+        return LLMIG_EINVAL;
+    std::lock_guard<std::mutex> lock(g_scratch_mutex);
+    if (!g_scratch_ptr[device]) {
+        void *p = nullptr;
+        const hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+        if (e != hipSuccess || !p)
+            return hip_error(e != hipSuccess ? e : hipErrorInvalidSymbol);
+        g_scratch_ptr[device] = p;
+    }
+    *out = g_scratch_ptr[device];
+    return LLMIG_OK;
 }
 
 bool same_geometry(const llmig_pool *a, const llmig_pool *b)
@@ -439,6 +472,11 @@ int llmig_pool_create(const llmig_pool_desc *desc, llmig_pool **out)
                 (void)hipFree(pool->d_tab);
             return hip_error(e);
         }
+        // Set-up of the scratch array's address on this device, so that the
+        // no-allocation entry point finds it ready; a failure here is
+        // reported by that entry point, which looks it up again.
+        void *unused = nullptr;
+        (void)scratch_pointer(pool->device, &unused);
         *out = pool.release();
         return LLMIG_OK;
     });
@@ -833,19 +871,18 @@ int llmig_stream_read(const void *region, int64_t bytes, int32_t passes, int32_t
     return e == hipSuccess ? LLMIG_OK : hip_error(e);
 }
 
-// Work items of a decode-attention call: one per partition of each sequence.
-static int attn_items(const int32_t *ctx_lens, int32_t batch, std::vector<int32_t> &seq,
-                      std::vector<int32_t> &start, std::vector<int32_t> &end)
+// Work items of a decode-attention call: one per partition of kPartTokens
+// tokens of each sequence, in sequence order.  LLMIG_EINVAL for a negative
+// length.
+static int attn_item_count(const int32_t *ctx_lens, int32_t batch, int64_t *n_items)
 {
+    int64_t n = 0;
     for (int32_t b = 0; b < batch; ++b) {
         if (ctx_lens[b] < 0)
             return LLMIG_EINVAL;
-        for (int32_t t = 0; t < ctx_lens[b]; t += kPartTokens) {
-            seq.push_back(b);
-            start.push_back(t);
-            end.push_back(std::min(ctx_lens[b], t + kPartTokens));
-        }
+        n += (static_cast<int64_t>(ctx_lens[b]) + kPartTokens - 1) / kPartTokens;
     }
+    *n_items = n;
     return LLMIG_OK;
 }
 
@@ -862,100 +899,147 @@ static int attn_workspace_bytes(int64_t num_layers, int64_t n_items, int64_t q_h
     return LLMIG_OK;
 }
 
+// Checks the arguments of a decode-attention call (all but the workspace);
+// on success gives the kernel, the item count and the workspace size.
+static int attn_check(const llmig_pool *pool, int32_t dtype, const void *q, int32_t batch, int32_t q_heads,
+                      const int32_t *tables, int32_t table_stride, const int32_t *ctx_lens, const float *out,
+                      const void **fn, int64_t *n_items, int64_t *ws_bytes)
+{
+    if (!pool || !on_current_device(pool) || (dtype != 0 && dtype != 1) || pool->elem_bytes != 2 || !q ||
+        !tables || !ctx_lens || !out || batch < 1 || batch > kAttnMaxBatch || q_heads < 1 || table_stride < 1 ||
+        pool->layouts[0] != LLMIG_LAYOUT_NHD || pool->layouts[1] != LLMIG_LAYOUT_NHD)
+        return LLMIG_EINVAL;
+    const int32_t hkv = pool->num_kv_heads;
+    if (q_heads % hkv != 0)
+        return LLMIG_EINVAL;
+    *fn = attn_kernel_for(dtype, pool->head_dim, q_heads / hkv);
+    if (!*fn || (reinterpret_cast<uintptr_t>(q) & 15u) || (reinterpret_cast<uintptr_t>(out) & 3u) ||
+        (reinterpret_cast<uintptr_t>(tables) & 3u))
+        return LLMIG_EINVAL;
+    for (int32_t b = 0; b < batch; ++b)
+        if (ctx_lens[b] < 0 || (ctx_lens[b] + pool->block_size - 1) / pool->block_size > table_stride)
+            return LLMIG_EINVAL;
+    if (attn_item_count(ctx_lens, batch, n_items) != LLMIG_OK || *n_items > 0x7fffffffLL)
+        return LLMIG_EINVAL;
+    return attn_workspace_bytes(pool->num_layers, *n_items, q_heads, pool->head_dim, ws_bytes);
+}
+
+// Enqueues a checked decode-attention call: the partial kernel over the
+// items, kAttnItems per launch (their ranges ride in the kernel arguments),
+// then the merge.  ws holds the partial results.  Allocates nothing.
+static int attn_enqueue(const llmig_pool *pool, const void *fn, const void *q, int32_t batch, int32_t q_heads,
+                        const int32_t *tables, int32_t table_stride, const int32_t *ctx_lens, float scale,
+                        float *ws, int64_t n_items, float *out, hipStream_t st)
+{
+    AttnArgs a;
+    std::memset(&a, 0, sizeof(a));
+    a.k_tab = pool->d_tab;
+    a.q = static_cast<const uint8_t *>(q);
+    a.tables = tables;
+    a.ws = ws;
+    a.scale = scale;
+    a.num_layers = static_cast<uint32_t>(pool->num_layers);
+    a.batch = static_cast<uint32_t>(batch);
+    a.q_heads = static_cast<uint32_t>(q_heads);
+    a.kv_heads = static_cast<uint32_t>(pool->num_kv_heads);
+    a.block_size = static_cast<uint32_t>(pool->block_size);
+    a.table_stride = static_cast<uint32_t>(table_stride);
+    a.n_items_total = static_cast<uint32_t>(n_items);
+    uint32_t m = 0, first = 0;
+    auto flush = [&]() -> hipError_t {
+        if (m == 0)
+            return hipSuccess;
+        a.item_base = first;
+        a.items = m;
+        void *args[] = {&a};
+        hipError_t e = hipLaunchKernel(fn, dim3(m * a.kv_heads, a.num_layers), dim3(kThreads), args, 0, st);
+        first += m;
+        m = 0;
+        return e;
+    };
+    for (int32_t b = 0; b < batch; ++b)
+        for (int32_t t = 0; t < ctx_lens[b]; t += kPartTokens) {
+            a.item_seq[m] = b;
+            a.item_start[m] = t;
+            a.item_end[m] = std::min(ctx_lens[b], t + kPartTokens);
+            if (++m == static_cast<uint32_t>(kAttnItems)) {
+                hipError_t e = flush();
+                if (e != hipSuccess)
+                    return hip_error(e);
+            }
+        }
+    hipError_t e = flush();
+    if (e != hipSuccess)
+        return hip_error(e);
+    AttnReduceArgs r;
+    std::memset(&r, 0, sizeof(r));
+    r.ws = ws;
+    r.out = out;
+    r.num_layers = a.num_layers;
+    r.batch = a.batch;
+    r.q_heads = a.q_heads;
+    r.head_dim = static_cast<uint32_t>(pool->head_dim);
+    r.n_items_total = a.n_items_total;
+    for (int32_t b = 0, i = 0; b < batch; ++b) {
+        r.seq_first[b] = i;
+        r.seq_count[b] = (ctx_lens[b] + kPartTokens - 1) / kPartTokens;
+        i += r.seq_count[b];
+    }
+    const uint64_t total = static_cast<uint64_t>(pool->num_layers) * batch * q_heads * pool->head_dim;
+    const uint32_t grid = static_cast<uint32_t>(std::min<uint64_t>((total + kThreads - 1) / kThreads, 1u << 20));
+    void *rargs[] = {&r};
+    e = hipLaunchKernel(reinterpret_cast<const void *>(&attn_reduce), dim3(grid), dim3(kThreads), rargs, 0, st);
+    return e == hipSuccess ? LLMIG_OK : hip_error(e);
+}
+
 int llmig_decode_attention_workspace(const int32_t *ctx_lens, int32_t batch, int32_t num_layers, int32_t q_heads,
                                      int32_t head_dim, int64_t *bytes)
 {
-    return no_throw([&]() -> int {
-        if (!bytes)
-            return LLMIG_EINVAL;
-        *bytes = 0;
-        if (!ctx_lens || batch < 1 || batch > kAttnMaxBatch || num_layers < 1 || q_heads < 1 || head_dim < 1)
-            return LLMIG_EINVAL;
-        std::vector<int32_t> seq, start, end;
-        if (attn_items(ctx_lens, batch, seq, start, end) != LLMIG_OK)
-            return LLMIG_EINVAL;
-        return attn_workspace_bytes(num_layers, static_cast<int64_t>(seq.size()), q_heads, head_dim, bytes);
-    });
+    if (!bytes)
+        return LLMIG_EINVAL;
+    *bytes = 0;
+    if (!ctx_lens || batch < 1 || batch > kAttnMaxBatch || num_layers < 1 || q_heads < 1 || head_dim < 1)
+        return LLMIG_EINVAL;
+    int64_t n_items = 0;
+    if (attn_item_count(ctx_lens, batch, &n_items) != LLMIG_OK)
+        return LLMIG_EINVAL;
+    return attn_workspace_bytes(num_layers, n_items, q_heads, head_dim, bytes);
 }
 
 int llmig_decode_attention(const llmig_pool *pool, int32_t dtype, const void *q, int32_t batch, int32_t q_heads,
                            const int32_t *tables, int32_t table_stride, const int32_t *ctx_lens, float scale,
                            void *workspace, int64_t workspace_bytes, float *out, void *stream)
 {
-    return no_throw([&]() -> int {
-        if (!pool || !on_current_device(pool) || (dtype != 0 && dtype != 1) || pool->elem_bytes != 2 || !q ||
-            !tables || !ctx_lens || !out ||
-            batch < 1 || batch > kAttnMaxBatch || q_heads < 1 || table_stride < 1 ||
-            pool->layouts[0] != LLMIG_LAYOUT_NHD || pool->layouts[1] != LLMIG_LAYOUT_NHD)
-            return LLMIG_EINVAL;
-        const int32_t D = pool->head_dim, hkv = pool->num_kv_heads;
-        if (q_heads % hkv != 0)
-            return LLMIG_EINVAL;
-        const void *fn = attn_kernel_for(dtype, D, q_heads / hkv);
-        if (!fn || (reinterpret_cast<uintptr_t>(q) & 15u) || (reinterpret_cast<uintptr_t>(out) & 3u) ||
-            (reinterpret_cast<uintptr_t>(tables) & 3u) || (reinterpret_cast<uintptr_t>(workspace) & 3u))
-            return LLMIG_EINVAL;
-        for (int32_t b = 0; b < batch; ++b)
-            if (ctx_lens[b] < 0 || (ctx_lens[b] + pool->block_size - 1) / pool->block_size > table_stride)
-                return LLMIG_EINVAL;
-        std::vector<int32_t> seq, start, end;
-        if (attn_items(ctx_lens, batch, seq, start, end) != LLMIG_OK)
-            return LLMIG_EINVAL;
-        const int64_t n_items = static_cast<int64_t>(seq.size());
-        int64_t need = 0;
-        if (attn_workspace_bytes(pool->num_layers, n_items, q_heads, D, &need) != LLMIG_OK ||
-            n_items > 0x7fffffffLL || (n_items > 0 && (!workspace || workspace_bytes < need)))
-            return LLMIG_EINVAL;
-        hipStream_t st = static_cast<hipStream_t>(stream);
+    const void *fn = nullptr;
+    int64_t n_items = 0, need = 0;
+    int rc = attn_check(pool, dtype, q, batch, q_heads, tables, table_stride, ctx_lens, out, &fn, &n_items, &need);
+    if (rc != LLMIG_OK)
+        return rc;
+    if ((reinterpret_cast<uintptr_t>(workspace) & 3u) || (n_items > 0 && (!workspace || workspace_bytes < need)))
+        return LLMIG_EINVAL;
+    return attn_enqueue(pool, fn, q, batch, q_heads, tables, table_stride, ctx_lens, scale,
+                        static_cast<float *>(workspace), n_items, out, static_cast<hipStream_t>(stream));
+}
 
-        AttnArgs a;
-        std::memset(&a, 0, sizeof(a));
-        a.k_tab = pool->d_tab;
-        a.q = static_cast<const uint8_t *>(q);
-        a.tables = tables;
-        a.ws = static_cast<float *>(workspace);
-        a.scale = scale;
-        a.num_layers = static_cast<uint32_t>(pool->num_layers);
-        a.batch = static_cast<uint32_t>(batch);
-        a.q_heads = static_cast<uint32_t>(q_heads);
-        a.kv_heads = static_cast<uint32_t>(hkv);
-        a.block_size = static_cast<uint32_t>(pool->block_size);
-        a.table_stride = static_cast<uint32_t>(table_stride);
-        a.n_items_total = static_cast<uint32_t>(n_items);
-        for (int64_t first = 0; first < n_items; first += kAttnItems) {
-            const int64_t m = std::min<int64_t>(kAttnItems, n_items - first);
-            a.item_base = static_cast<uint32_t>(first);
-            a.items = static_cast<uint32_t>(m);
-            std::memcpy(a.item_seq, seq.data() + first, m * sizeof(int32_t));
-            std::memcpy(a.item_start, start.data() + first, m * sizeof(int32_t));
-            std::memcpy(a.item_end, end.data() + first, m * sizeof(int32_t));
-            void *args[] = {&a};
-            hipError_t e = hipLaunchKernel(fn, dim3(static_cast<uint32_t>(m * hkv), a.num_layers), dim3(kThreads), args,
-                                           0, st);
-            if (e != hipSuccess)
-                return hip_error(e);
-        }
-        AttnReduceArgs r;
-        std::memset(&r, 0, sizeof(r));
-        r.ws = static_cast<const float *>(workspace);
-        r.out = out;
-        r.num_layers = a.num_layers;
-        r.batch = a.batch;
-        r.q_heads = a.q_heads;
-        r.head_dim = static_cast<uint32_t>(D);
-        r.n_items_total = a.n_items_total;
-        for (int64_t i = 0, b = 0; b < batch; ++b) {
-            r.seq_first[b] = static_cast<int32_t>(i);
-            while (i < n_items && seq[i] == b)
-                ++i;
-            r.seq_count[b] = static_cast<int32_t>(i) - r.seq_first[b];
-        }
-        const uint64_t total = static_cast<uint64_t>(pool->num_layers) * batch * q_heads * D;
-        const uint32_t grid = static_cast<uint32_t>(std::min<uint64_t>((total + kThreads - 1) / kThreads, 1u << 20));
-        void *rargs[] = {&r};
-        hipError_t e = hipLaunchKernel(reinterpret_cast<const void *>(&attn_reduce), dim3(grid), dim3(kThreads), rargs, 0,
-                                       st);
-        return e == hipSuccess ? LLMIG_OK : hip_error(e);
+int llmig_decode_attention_noalloc(const llmig_pool *pool, int32_t dtype, const void *q, int32_t batch,
+                                   int32_t q_heads, const int32_t *tables, int32_t table_stride,
+                                   const int32_t *ctx_lens, float scale, float *out, void *stream)
+{
+    return no_throw([&]() -> int { // the mutex is the only thing here that could throw
+        const void *fn = nullptr;
+        int64_t n_items = 0, need = 0;
+        int rc = attn_check(pool, dtype, q, batch, q_heads, tables, table_stride, ctx_lens, out, &fn, &n_items,
+                            &need);
+        if (rc != LLMIG_OK)
+            return rc;
+        if (need > static_cast<int64_t>(LLMIG_DECODE_SCRATCH_BYTES))
+            return LLMIG_ESCRATCH;
+        void *ws = nullptr;
+        rc = scratch_pointer(pool->device, &ws);
+        if (rc != LLMIG_OK)
+            return rc;
+        return attn_enqueue(pool, fn, q, batch, q_heads, tables, table_stride, ctx_lens, scale,
+                            static_cast<float *>(ws), n_items, out, static_cast<hipStream_t>(stream));
     });
 }
 
@@ -972,6 +1056,8 @@ const char *llmig_strerror(int code)
         return "block id out of range";
     case LLMIG_EHIP:
         return "HIP runtime error";
+    case LLMIG_ESCRATCH:
+        return "the call needs more than the library's static scratch array (LLMIG_DECODE_SCRATCH_BYTES) holds";
     default:
         return "unknown error";
     }

@@ -22,8 +22,10 @@ if not os.path.exists(LIBRARY):
 
 _lib = ctypes.CDLL(LIBRARY)
 
-LLMIG_OK, LLMIG_EINVAL, LLMIG_ENOSPC, LLMIG_ERANGE, LLMIG_EHIP = 0, -1, -2, -3, -4
-ERROR_NAMES = {0: "OK", -1: "EINVAL", -2: "ENOSPC", -3: "ERANGE", -4: "EHIP"}
+LLMIG_OK, LLMIG_EINVAL, LLMIG_ENOSPC, LLMIG_ERANGE, LLMIG_EHIP, LLMIG_ESCRATCH = 0, -1, -2, -3, -4, -5
+ERROR_NAMES = {0: "OK", -1: "EINVAL", -2: "ENOSPC", -3: "ERANGE", -4: "EHIP", -5: "ESCRATCH"}
+# Bytes of the static array behind llmig_decode_attention_noalloc (LLMIG_DECODE_SCRATCH_BYTES).
+DECODE_SCRATCH_BYTES = 32 << 20
 
 
 class LlmigError(RuntimeError):
@@ -101,6 +103,9 @@ _lib.llmig_decode_attention_workspace.restype = ctypes.c_int
 _lib.llmig_decode_attention.argtypes = [_vp, ctypes.c_int32, _vp, ctypes.c_int32, ctypes.c_int32, _vp,
                                         ctypes.c_int32, _vp, ctypes.c_float, _vp, ctypes.c_int64, _vp, _vp]
 _lib.llmig_decode_attention.restype = ctypes.c_int
+_lib.llmig_decode_attention_noalloc.argtypes = [_vp, ctypes.c_int32, _vp, ctypes.c_int32, ctypes.c_int32, _vp,
+                                                ctypes.c_int32, _vp, ctypes.c_float, _vp, _vp]
+_lib.llmig_decode_attention_noalloc.restype = ctypes.c_int
 _lib.llmig_strerror.argtypes = [ctypes.c_int]
 _lib.llmig_strerror.restype = ctypes.c_char_p
 _lib.llmig_last_hip_error.argtypes = []
@@ -363,11 +368,7 @@ def decode_workspace_bytes(ctx_lens, num_layers: int, q_heads: int, head_dim: in
     return n.value
 
 
-def llmig_decode_attention(pool: Pool, q: torch.Tensor, tables: torch.Tensor, ctx_lens, scale: float,
-                           workspace: torch.Tensor, out: torch.Tensor, stream=None) -> None:
-    """Decode attention over ``pool`` (the work beside a migration).  q: CUDA
-    [L][B][Hq][D] fp16/bf16; tables: CUDA int32 [B][stride]; ctx_lens: host
-    lengths; out: CUDA float32 [L][B][Hq][D]."""
+def _attention_args(pool: Pool, q: torch.Tensor, tables: torch.Tensor, ctx_lens, out: torch.Tensor) -> np.ndarray:
     if q.dtype not in (torch.float16, torch.bfloat16) or not q.is_cuda or not q.is_contiguous():
         raise ValueError("q must be a contiguous CUDA fp16/bf16 tensor")
     if q.dim() != 4 or q.shape[0] != pool.num_layers or q.shape[3] != pool.head_dim or q.dtype != pool.k[0].dtype:
@@ -376,11 +377,20 @@ def llmig_decode_attention(pool: Pool, q: torch.Tensor, tables: torch.Tensor, ct
         raise ValueError("tables must be a contiguous CUDA int32 [batch][stride] tensor")
     if out.dtype != torch.float32 or not out.is_cuda or not out.is_contiguous() or out.shape != q.shape:
         raise ValueError("out must be a contiguous CUDA float32 tensor shaped like q")
-    if not workspace.is_cuda or not workspace.is_contiguous():
-        raise ValueError("workspace must be a contiguous CUDA tensor")
     c = _host_i32(ctx_lens)
     if c.size != q.shape[1] or tables.shape[0] < q.shape[1]:
         raise ValueError("ctx_lens must hold one length per sequence of q, tables one row each")
+    return c
+
+
+def llmig_decode_attention(pool: Pool, q: torch.Tensor, tables: torch.Tensor, ctx_lens, scale: float,
+                           workspace: torch.Tensor, out: torch.Tensor, stream=None) -> None:
+    """Decode attention over ``pool`` (the work beside a migration).  q: CUDA
+    [L][B][Hq][D] fp16/bf16; tables: CUDA int32 [B][stride]; ctx_lens: host
+    lengths; out: CUDA float32 [L][B][Hq][D]."""
+    c = _attention_args(pool, q, tables, ctx_lens, out)
+    if not workspace.is_cuda or not workspace.is_contiguous():
+        raise ValueError("workspace must be a contiguous CUDA tensor")
     _check(_lib.llmig_decode_attention(pool.handle, 1 if q.dtype == torch.bfloat16 else 0, q.data_ptr(),
                                        q.shape[1], q.shape[2], tables.data_ptr(), tables.shape[1],
                                        c.ctypes.data, float(scale), workspace.data_ptr(),
@@ -397,3 +407,15 @@ def llmig_stream_read(region: torch.Tensor, passes: int, workgroups: int, out: t
     _check(_lib.llmig_stream_read(region.data_ptr(), region.numel() * region.element_size(), int(passes),
                                   int(workgroups), out.data_ptr(), out.numel(), _stream(stream)),
            "llmig_stream_read")
+
+
+def llmig_decode_attention_noalloc(pool: Pool, q: torch.Tensor, tables: torch.Tensor, ctx_lens, scale: float,
+                                   out: torch.Tensor, stream=None) -> None:
+    """llmig_decode_attention with its partial results in the library's
+    static device array (for callers that cannot allocate); raises
+    LlmigError ESCRATCH when they need more than DECODE_SCRATCH_BYTES."""
+    c = _attention_args(pool, q, tables, ctx_lens, out)
+    _check(_lib.llmig_decode_attention_noalloc(pool.handle, 1 if q.dtype == torch.bfloat16 else 0, q.data_ptr(),
+                                               q.shape[1], q.shape[2], tables.data_ptr(), tables.shape[1],
+                                               c.ctypes.data, float(scale), out.data_ptr(), _stream(stream)),
+           "llmig_decode_attention_noalloc")

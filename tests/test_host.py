@@ -41,7 +41,7 @@ def test_error_codes_match_header():
     codes = {m[0]: int(m[1]) for m in re.findall(r"#define (LLMIG_\w+) \((-?\d+)\)", text)}
     codes.update({m[0]: int(m[1]) for m in re.findall(r"#define (LLMIG_OK) (\d+)", text)})
     assert codes == {"LLMIG_OK": 0, "LLMIG_EINVAL": -1, "LLMIG_ENOSPC": -2, "LLMIG_ERANGE": -3,
-                     "LLMIG_EHIP": -4}
+                     "LLMIG_EHIP": -4, "LLMIG_ESCRATCH": -5}
     for name, code in codes.items():
         assert llmig.ERROR_NAMES[code] == name[len("LLMIG_"):]
         assert llmig._lib.llmig_strerror(code)
@@ -124,6 +124,8 @@ def test_enqueue_calls_reject_bad_arguments_without_gpu():
     assert lib.llmig_unpack_layout(None, None, 0, 0, None, 0, 1, 3, None) == llmig.LLMIG_EINVAL
     assert lib.llmig_unpack_layout(None, None, 0, 0, None, 0, 4, 0, None) == llmig.LLMIG_EINVAL
     assert lib.llmig_write_tokens(None, None, 0, 0, 0, None, None) == llmig.LLMIG_EINVAL
+    assert lib.llmig_decode_attention_noalloc(None, 0, None, 1, 1, None, 1, None, 1.0, None,
+                                              None) == llmig.LLMIG_EINVAL
     assert lib.llmig_pool_create(None, None) == llmig.LLMIG_EINVAL
     out = ctypes.c_void_p(1)
     assert lib.llmig_pool_create(None, ctypes.byref(out)) == llmig.LLMIG_EINVAL and not out.value

@@ -1,0 +1,85 @@
+"""The entry point for callers that cannot allocate: decode attention with its
+partial results in the library's static device array
+(llmig_decode_attention_noalloc), through the C ABI.
+
+Two calls in a row, the second smaller than the first (so the array holds
+the first call's entries past the second's), each bit-identical to
+llmig_decode_attention on a fresh workspace filled with NaN patterns (the
+same kernels, so the same arithmetic) and within the oracle's error bound;
+a call too large for the array is refused and leaves its output alone."""
+import sys
+
+import numpy as np
+import pytest
+import torch
+
+import attn_cases as ac
+from paper_2406_03243_amd import harness
+from paper_2406_03243_amd import workloads as wl
+
+pytestmark = pytest.mark.gpu
+
+if torch.cuda.is_available():
+    from paper_2406_03243_amd.llmig import (DECODE_SCRATCH_BYTES, LLMIG_ESCRATCH, LlmigError, Pool,
+                                            decode_workspace_bytes, llmig_decode_attention,
+                                            llmig_decode_attention_noalloc)
+
+
+def say(*a):
+    print("[case]", *a, flush=True)
+    sys.stdout.flush()
+
+
+def _run(case, seed):
+    num_layers, num_blocks, bs, kv_heads, head_dim, group, ctx, dtype, _ = case
+    host, qbits, tables, ctx, scale = ac.case_inputs(case, seed)
+    shape = wl.PoolShape(num_layers, num_blocks, bs, kv_heads, head_dim, dtype)
+    k, v = harness.alloc_layers(shape)
+    for t, a in zip(k + v, host.k + host.v):
+        harness.tile_view(t).copy_(torch.from_numpy(a))
+    pool = Pool(k, v)
+    q = torch.from_numpy(qbits.view(np.int16)).view(harness.TORCH_DTYPE[dtype]).cuda()
+    tab = torch.from_numpy(tables).cuda()
+    q_heads = kv_heads * group
+    ws = torch.full((max(1, decode_workspace_bytes(ctx, num_layers, q_heads, head_dim)),), 0xFF,
+                    dtype=torch.uint8, device="cuda")
+    ref = torch.full(q.shape, float("nan"), dtype=torch.float32, device="cuda")
+    got = torch.full(q.shape, float("nan"), dtype=torch.float32, device="cuda")
+    llmig_decode_attention(pool, q, tab, ctx, scale, ws, ref)
+    llmig_decode_attention_noalloc(pool, q, tab, ctx, scale, got)
+    torch.cuda.synchronize()
+    ref_h, got_h = ref.cpu().numpy(), got.cpu().numpy()
+    assert np.array_equal(ref_h.view(np.uint32), got_h.view(np.uint32)), "differs from llmig_decode_attention"
+    orc = ac.default_oracle()
+    want = orc.decode_attention(host, kv_heads, head_dim, dtype, qbits, tables, ctx, scale)
+    tol = ac.tolerance(orc, host, kv_heads, head_dim, dtype, qbits, tables, ctx, scale)
+    ratio = ac.excess(got_h, want, tol)
+    say(f"items {len(ac.items(ctx))} x {num_layers} layers: bit-identical to the workspace call, "
+        f"max error / bound {ratio.max():.3g}")
+    assert (ratio <= 1.0).all()
+
+
+def test_noalloc_matches_workspace_call_twice():
+    first = (2, 400, 16, 2, 128, 4, [1500, 700, 3000], "bf16", False)
+    second = (1, 100, 16, 2, 64, 2, [300, 900], "fp16", False)
+    say("noalloc: first call", first)
+    _run(first, 4242)
+    say("noalloc: second, smaller call", second)
+    _run(second, 4243)
+
+
+def test_noalloc_refuses_a_call_too_large_for_the_array():
+    say("noalloc: too large")
+    shape = wl.PoolShape(1, 20, 16, 1, 128, "fp16")
+    k, v = harness.alloc_layers(shape)
+    pool = Pool(k, v)
+    q = torch.zeros((1, 1, 16, 128), dtype=torch.float16, device="cuda")
+    ctx = [4_200_000]                                        # 4102 partitions x 16 heads x 130 floats
+    assert decode_workspace_bytes(ctx, 1, 16, 128) > DECODE_SCRATCH_BYTES
+    tab = torch.zeros((1, -(-ctx[0] // 16)), dtype=torch.int32, device="cuda")
+    out = torch.full(q.shape, 7.0, dtype=torch.float32, device="cuda")
+    with pytest.raises(LlmigError) as e:
+        llmig_decode_attention_noalloc(pool, q, tab, ctx, 1.0, out)
+    assert e.value.code == LLMIG_ESCRATCH
+    torch.cuda.synchronize()
+    assert bool((out == 7.0).all())
