@@ -110,7 +110,6 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
-    ap.add_argument("--cpu-seconds", type=float, default=10.0, help="CPU oracle sample budget")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--sections", default="downtime,batched,load,xlayout",
                     help="extra workloads after the main one (comma list of downtime, batched, load, xlayout;"
@@ -197,13 +196,16 @@ def main():
     downtimes = [d for _, d in runs]
     kernel_name = "copy_tiles<0, 0, %d, %d>" % (ids_mode, bulk_span_rows(src.tile_bytes))
 
-    # GPU time of the final stage's copy alone (events around its launch), in
-    # extra steps outside the timed region: the host downtime above also
-    # holds its planning, launch and the host's view of completion.
-    final_gpu = []
+    # GPU time of every stage's copy (events around its launches), in extra
+    # migrations outside the timed region: within the timed steps only stage
+    # 1 carries events, since events around the later stages would add their
+    # host work to the step (and to the final stage's downtime).
+    extra = []
     for _ in range(max(args.steps, 10)):
-        mf, _ = migrate.run_scheduled(src, dst, table, free, initial, appends, mig, dec, time_final=True)
-        final_gpu.append(mf.stages[-1].gpu_us)
+        mf, _ = migrate.run_scheduled(src, dst, table, free, initial, appends, mig, dec, time_all=True,
+                                      time_final=True)
+        extra.append(mf)
+    final_gpu = [mf.stages[-1].gpu_us for mf in extra]
 
     # The same launch on contiguous tiles (block i of every layer tensor to
     # block i, as many blocks as stage 1), outside the timed region: what
@@ -224,12 +226,14 @@ def main():
     stages = []
     for i, rec in enumerate(m0.stages):
         us = [m.stages[i].gpu_us for m, _ in runs if m.stages[i].gpu_us > 0]
+        timed_in = "timed steps"
+        if not us:
+            us = [mf.stages[i].gpu_us for mf in extra]
+            timed_in = "extra migrations after the timed steps"
         b = stage_bytes(rec.blocks, shape, src.tile_bytes)
-        entry = {"tokens": [rec.from_tok, rec.to_tok], "blocks": rec.blocks, "bytes": b, "final": rec.final}
-        if us:
-            entry["gpu_us_median"] = round(statistics.median(us), 2)
-            entry["gpu_us"] = spread(us)
-            entry["GBps"] = round(b / (statistics.median(us) * 1e-6) / 1e9, 1)
+        entry = {"tokens": [rec.from_tok, rec.to_tok], "blocks": rec.blocks, "bytes": b, "final": rec.final,
+                 "gpu_us_median": round(statistics.median(us), 2), "gpu_us": spread(us),
+                 "GBps": round(b / (statistics.median(us) * 1e-6) / 1e9, 1), "timed_in": timed_in}
         stages.append(entry)
 
     result = {
@@ -279,7 +283,12 @@ def main():
 
     # ------------------------------------------------------------------ CPU oracle baseline
     if not args.no_cpu_baseline:
-        result["cpu_baseline"] = cpu_baseline(src, table, free, m0.stages[0], shape, args.cpu_seconds)
+        from paper_2406_03243_amd.llmig import llmig_plan
+        s1 = m0.stages[0]
+        ms1, _ = llmig_plan(table, free, s1.length, s1.from_tok, s1.to_tok, src.block_size)
+        result["cpu_baseline"] = cpu_baseline(
+            src, ms1[:CPU_SAMPLE_PAIRS], shape,
+            f"{CPU_SAMPLE_PAIRS} of the {s1.blocks} stage-1 block pairs of {w.name}")
 
     if args.calibration_copy:
         a = torch.empty(1 << 30, dtype=torch.uint8, device=dev)
@@ -300,7 +309,7 @@ def main():
         result["downtime_vs_len"] = downtime_sweep(args.downtime_reps)
         torch.cuda.empty_cache()
     if "batched" in sections:
-        result["batched"] = batched_section()
+        result["batched"] = batched_section(cpu=not args.no_cpu_baseline)
         torch.cuda.empty_cache()
     if "load" in sections:
         result["under_load"] = load_section()
@@ -312,54 +321,66 @@ def main():
     print(json.dumps(result), flush=True)
 
 
-def cpu_baseline(src, table, free, stage1, shape, seconds):
-    """The oracle's per-tile copy on host snapshots of a sample of stage 1's
-    blocks: one thread for 0.4 x ``seconds``, then every core of the
-    process's CPU share (at most 16) on disjoint slices, about 2 x
-    ``seconds`` of CPU work in all.  ``value`` is the all-core rate."""
+# CPU baseline: the oracle's block-by-block copy on host snapshots of a sample
+# of a stage's block pairs.  The sample holds the mapped source blocks only (a
+# compact pool behind an id remap) and a zeroed destination of the same size.
+CPU_SAMPLE_PAIRS = 256
+CPU_WARMUP_RUNS = 3
+CPU_TIMED_RUNS = 5
+# Threads of the all-core leg: the process's CPU affinity, capped at the CPU
+# share a one-GPU job gets on the GPU machines (16 CPUs), where the affinity
+# mask can name the whole host.
+CPU_SHARE = 16
+
+
+def cpu_baseline(src, ids, shape, what):
+    """The oracle's per-tile copy of the pairs whose source blocks are
+    ``ids``, on host snapshots: one thread, then every CPU of the process's
+    share on disjoint slices.  Each leg runs CPU_WARMUP_RUNS untimed runs and
+    reports the median of CPU_TIMED_RUNS timed ones; a single-thread run is
+    one pass over the sample, an all-core run one pass per thread over each
+    thread's slice (the same bytes per thread as one pass over the sample).
+    ``value`` is the all-core rate."""
     import numpy as np
+    from concurrent.futures import ThreadPoolExecutor
 
     import oracle
     from oracle import HostPool
     from paper_2406_03243_amd import harness
 
-    from paper_2406_03243_amd.llmig import llmig_plan
-
-    n = 64
-    ms, md = llmig_plan(table, free, stage1.length, stage1.from_tok, stage1.to_tok, src.block_size)
-    ms, md = ms[:n], md[:n]
-    hs = HostPool(harness.snapshot_blocks(src.k, ms), harness.snapshot_blocks(src.v, ms),
+    ids = np.asarray(ids, np.int32)
+    n = len(ids)
+    hs = HostPool(harness.snapshot_blocks(src.k, ids), harness.snapshot_blocks(src.v, ids),
                   src.block_size, src.slot_bytes)
     hd = HostPool.zeros(shape.num_layers, n, src.block_size, src.slot_bytes)
-    ids = np.arange(n, dtype=np.int32)
+    local = np.arange(n, dtype=np.int32)
     orc = oracle.default()
-    orc.copy(hs, hd, ids, ids)           # warm the pages
-    per_pair = 2 * shape.num_layers * 2 * src.tile_bytes
+    per_pair = 2 * shape.num_layers * 2 * src.tile_bytes      # read + written
 
-    def timed(chunk, budget):
-        reps, t0 = 0, time.perf_counter()
-        while True:
-            orc.copy(hs, hd, chunk, chunk)
-            reps += 1
-            el = time.perf_counter() - t0
-            if el >= budget:
-                return reps, el
+    def leg(threads):
+        chunks = np.array_split(local, threads)
+        passes = threads if threads > 1 else 1
 
-    # one thread
-    reps1, el1 = timed(ids, 0.4 * seconds)
-    single = reps1 * n * per_pair / el1 / 1e9
-    # every core of the process's CPU share (at most 16), each thread on its
-    # own slice of the pairs; the C oracle runs outside the interpreter lock
-    threads = max(1, min(16, len(os.sched_getaffinity(0)), n))
-    chunks = np.array_split(ids, threads)
-    budget = max(1.0, 2.0 * seconds / threads)     # about 2 x seconds of CPU work over all threads
-    from concurrent.futures import ThreadPoolExecutor
-    t0 = time.perf_counter()
-    with ThreadPoolExecutor(max_workers=threads) as ex:
-        res = list(ex.map(lambda c: (timed(c, budget), len(c)), chunks))
-    wall = time.perf_counter() - t0
-    moved = sum(r * k * per_pair for (r, _), k in res)
-    multi = moved / wall / 1e9
+        def work(c):
+            for _ in range(passes):
+                orc.copy(hs, hd, c, c)
+
+        rates = []
+        with ThreadPoolExecutor(max_workers=threads) as ex:
+            for r in range(CPU_WARMUP_RUNS + CPU_TIMED_RUNS):
+                t0 = time.perf_counter()
+                list(ex.map(work, chunks))
+                el = time.perf_counter() - t0
+                if r >= CPU_WARMUP_RUNS:
+                    rates.append(passes * n * per_pair / el / 1e9)
+        return {"value": round(statistics.median(rates), 2), "unit": "GB/s", "cores": threads,
+                "runs_GBps": [round(x, 2) for x in rates], "warmup_runs": CPU_WARMUP_RUNS,
+                "bytes_per_run": passes * n * per_pair}
+
+    affinity = len(os.sched_getaffinity(0))
+    threads = max(1, min(CPU_SHARE, affinity, n))
+    single = leg(1)
+    multi = leg(threads)
     model = ""
     try:
         for line in open("/proc/cpuinfo"):
@@ -368,13 +389,13 @@ def cpu_baseline(src, table, free, stage1, shape, seconds):
                 break
     except OSError:
         pass
-    return {"value": round(multi, 2), "unit": "GB/s", "cores": threads, "kind": "oracle",
-            "sample": f"{n} of the {stage1.blocks} stage-1 block pairs (all {shape.num_layers} layers, "
-                      f"K and V, {n * shape.num_layers * 2} tiles of {src.tile_bytes} B) copied from host "
-                      f"snapshots by the oracle's per-tile memcpy: {threads} threads on disjoint slices for "
-                      f"{wall:.1f} s",
-            "single_thread": {"value": round(single, 2), "unit": "GB/s", "cores": 1, "seconds": round(el1, 1),
-                              "reps": reps1},
+    return {"value": multi["value"], "unit": "GB/s", "cores": threads, "kind": "oracle",
+            "sample": f"{what}: all {shape.num_layers} layers, K and V, {n * shape.num_layers * 2} tiles of "
+                      f"{src.tile_bytes} B, copied from host snapshots (a compact pool of the mapped blocks) by "
+                      f"the oracle's per-tile memcpy; median of {CPU_TIMED_RUNS} runs after {CPU_WARMUP_RUNS} "
+                      f"warm-ups per leg",
+            "all_cores": multi, "single_thread": single,
+            "affinity_cpus": affinity, "nproc": os.cpu_count(), "cpu_share_cap": CPU_SHARE,
             "cpu_model": model}
 
 
@@ -435,11 +456,12 @@ def downtime_sweep(reps):
     return out
 
 
-def batched_section(reps=20, host_reps=3, chunk_pairs=64):
+def batched_section(reps=20, host_reps=3, chunk_pairs=64, cpu=True):
     """64 requests migrated in one llmig_stage call; the same pairs packed
     into and unpacked from device staging (block fusion's kernels alone);
     and the same pairs through pinned host memory (pack -> host -> unpack,
     chunked, two buffers), then each direction alone."""
+    import numpy as np
     import torch
 
     from paper_2406_03243_amd import harness, migrate, scenarios
@@ -538,6 +560,13 @@ def batched_section(reps=20, host_reps=3, chunk_pairs=64):
         out["host_staged"][name] = {"seconds_median": round(t, 4), "GBps": round(gbs, 2),
                                     "link_frac": round(gbs / PCIE_GBS, 3)}
     log("batched host staged", out["host_staged"])
+    if cpu:
+        # the oracle on a compact sample of the batched pairs, evenly spaced
+        # over the concatenated mapping (so over all 64 requests)
+        pick = ms[np.linspace(0, len(ms) - 1, CPU_SAMPLE_PAIRS).astype(np.int64)]
+        out["cpu_baseline"] = cpu_baseline(src, pick, shape,
+                                           f"{CPU_SAMPLE_PAIRS} of the {len(ms)} batched block pairs "
+                                           f"(evenly spaced over the 64 requests)")
     su.close()
     return out
 

@@ -285,6 +285,7 @@ class MigrationHandle:
         _check(_lib.llmig_migration_create(int(block_size), ctypes.byref(h)), "llmig_migration_create")
         self._h = h
         self.block_size = int(block_size)
+        self._copied = ctypes.c_int64(0)
 
     def close(self):
         if getattr(self, "_h", None) is not None and _lib is not None:
@@ -308,6 +309,12 @@ class MigrationHandle:
                 e.record(torch.cuda.current_stream())
         _check(_lib.llmig_migration_set_stage_events(self._h, start.cuda_event, stop.cuda_event),
                "llmig_migration_set_stage_events")
+
+    def copied_tokens(self) -> int:
+        """Tokens the stages so far have copied (the coordinator's own count)."""
+        _check(_lib.llmig_migration_info(self._h, None, ctypes.byref(self._copied), None, None),
+               "llmig_migration_info")
+        return self._copied.value
 
     def info(self):
         st, cp, rs, ns = ctypes.c_int32(), ctypes.c_int64(), ctypes.c_int64(), ctypes.c_int64()

@@ -52,12 +52,15 @@ class Migration:
     """One request's migration, driven through the library's coordinator
     (which plans, reserves destination blocks and launches each stage in one
     call).  Keeps the host-side records: the stages so far, their GPU times,
-    and which destination blocks were consumed from the free list."""
+    and which destination blocks were consumed from the free list.  A
+    stage's token range is the coordinator's: it starts where the previous
+    stage ended and ends at the coordinator's count of copied tokens after
+    the call, so the records cannot drift from what the library reserved."""
 
     def __init__(self, src: Pool, dst: Pool, src_table, dst_free_list, stream: torch.cuda.Stream,
-                 max_workgroups: int = 0):
+                 max_workgroups: int = 0, block_size: int | None = None):
         self.src, self.dst, self.stream = src, dst, stream
-        self.bs = src.block_size
+        self.bs = src.block_size if block_size is None else int(block_size)
         self.src_table = np.ascontiguousarray(np.asarray(src_table, dtype=np.int32))
         self._free0 = np.ascontiguousarray(np.asarray(dst_free_list, dtype=np.int32))
         self._consumed = 0
@@ -80,12 +83,23 @@ class Migration:
         return self._free0[:self._consumed]
 
     def remaining_blocks(self, length: int) -> int:
+        """Blocks of a request now holding ``length`` tokens that no stage
+        has copied yet (the input of the driver's decision to end)."""
         return math.ceil(length / self.bs) - self.copied_tok // self.bs
+
+    def _record(self, length: int, n: int, final: bool, ev) -> StageRecord:
+        to_tok = self.coord.copied_tokens()
+        rec = StageRecord(length, self.copied_tok, to_tok, n, final)
+        self.stages.append(rec)
+        self._events.append(ev)
+        self._consumed += n
+        self.copied_tok = to_tok
+        return rec
 
     def stage(self, length: int, final: bool, time_it: bool = True) -> StageRecord:
         """Plan, reserve and launch the next stage for a request that now
-        holds ``length`` tokens.  A non-final stage stops at the last whole
-        block."""
+        holds ``length`` tokens (a non-final stage stops at the last whole
+        block: the coordinator's rule)."""
         ev = None
         if time_it:
             # recorded by the library right around its launches: kernel time
@@ -100,13 +114,13 @@ class Migration:
         if time_it and n == 0:
             _spare_timers.append(ev)    # not recorded by the library: free again
             ev = None
-        end = length if final else (length // self.bs) * self.bs
-        rec = StageRecord(length, self.copied_tok, end, n, final)
-        self.stages.append(rec)
-        self._events.append(ev)
-        self._consumed += n
-        self.copied_tok = end
-        return rec
+        return self._record(length, n, final, ev)
+
+    def plan(self, length: int, final: bool):
+        """The same step without the copy (host only): reserve and plan the
+        next stage.  Returns (record, map_src, map_dst)."""
+        ms, md = self.coord.next(self.src_table, length, final, self.free)
+        return self._record(length, len(md), final, None), ms, md
 
     def abort(self) -> np.ndarray:
         """Abort: the destination blocks reserved so far, to be released."""
