@@ -431,10 +431,9 @@ def downtime_sweep(reps):
             mm = migrate.Migration(src, dst, table, free, mig)
             torch.cuda.synchronize()
             t0 = time.perf_counter()
-            mm.stage(length, final=True, time_it=False)
-            mig.synchronize()
+            mm.finish(length)
             if r:
-                blocking.append((time.perf_counter() - t0) * 1e6)
+                blocking.append((mm.finished_at - t0) * 1e6)
         s1 = [m.stages[0] for m, _ in res]
         s1_us = statistics.median(s.gpu_us for s in s1)
         s1_bytes = stage_bytes(s1[0].blocks, shape, src.tile_bytes)

@@ -283,6 +283,23 @@ int llmig_migration_stage(llmig_migration *m, const llmig_pool *src, const llmig
                           const int32_t *src_table, int64_t src_table_len, int64_t len, int final_stage,
                           const int32_t *dst_free_list, int64_t dst_free_len, void *stream, int64_t *out_n);
 
+/* The final stage (§4.2: the request has been drained from its batch and
+ * what is left is copied; only this stage is downtime): llmig_migration_stage
+ * with final_stage = 1, followed by a wait until `stream` has finished all
+ * its work, so that on LLMIG_OK the request's whole KV cache is in the
+ * destination pool when the call returns (the caller may commit and resume
+ * the request there).  One call keeps the downtime path free of any host
+ * work between the launch and the wait.  The wait ends as soon as possible:
+ * behind the copy a one-lane kernel stores a ticket into pinned host memory
+ * that the library allocated with the first pool, and the calling thread
+ * reads it without calling the runtime, for up to 2 ms, before it falls
+ * back to hipStreamSynchronize (so the thread spins while it waits).
+ * Errors as llmig_migration_stage; a failed wait is LLMIG_EHIP (the stage's
+ * blocks stay reserved). */
+int llmig_migration_finish(llmig_migration *m, const llmig_pool *src, const llmig_pool *dst,
+                           const int32_t *src_table, int64_t src_table_len, int64_t len,
+                           const int32_t *dst_free_list, int64_t dst_free_len, void *stream, int64_t *out_n);
+
 /* Caps the number of workgroups the migration's non-final stages launch
  * (0, the default, means one per work item); the final stage is the
  * request's downtime and always runs uncapped.  A capped grid keeps fewer workgroups

@@ -14,6 +14,8 @@
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
+#include <atomic>
+#include <chrono>
 #include <cstdint>
 #include <cstring>
 #include <memory>
@@ -149,6 +151,16 @@ __global__ void __launch_bounds__(kThreads) stream_read_words(const uint8_t *reg
     ((LLMIG_GLOBAL uint64_t *)out)[lane] = folded;
 }
 
+// Completion signal of llmig_migration_finish: one lane stores the call's
+// ticket into its slot of pinned host memory, a release store at system
+// scope (a vector store), once the stream's earlier work (the final stage's
+// copy) has completed.
+__global__ void __launch_bounds__(64) signal_host(uint64_t *slot, uint64_t ticket)
+{
+    if (threadIdx.x == 0)
+        __hip_atomic_store(slot, ticket, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_SYSTEM);
+}
+
 // Runs an entry point's body.  The host code's only exceptions are failed
 // allocations (the id bitmaps, plan scratch, pool bookkeeping); they become
 // LLMIG_EINVAL here instead of crossing the C ABI.  Bodies allocate before
@@ -193,6 +205,82 @@ int scratch_pointer(int device, void **out)
     }
     *out = g_scratch_ptr[device];
     return LLMIG_OK;
+}
+
+// Host-visible completion slots of llmig_migration_finish: kFinishSlots
+// 64-bit tickets, one cache line apart, in pinned host memory mapped for
+// every device, allocated with the first pool (set-up) and kept for the
+// process.  Each call takes the next ticket from a counter; its slot is
+// ticket % kFinishSlots, and a slot only ever receives larger tickets.
+constexpr uint64_t kFinishSlots = 1024;
+constexpr uint64_t kFinishSlotStride = 64 / sizeof(uint64_t);
+// How long llmig_migration_finish reads its slot before it falls back to a
+// runtime wait on the stream (a final stage behind other queued work can
+// take longer than this).
+constexpr double kFinishSpinUs = 2000.0;
+
+struct FinishSlots {
+    std::mutex mu;                             // serialises the set-up
+    std::atomic<uint64_t *> host{nullptr};
+    std::atomic<uint64_t *> dev[kMaxDevices] = {};
+    std::atomic<uint64_t> next{1};
+};
+FinishSlots g_finish;
+
+// Allocates the slots (once) and maps them for `device` (current).
+void finish_slots_setup(int device)
+{
+    if (device < 0 || device >= kMaxDevices)
+        return;
+    std::lock_guard<std::mutex> lock(g_finish.mu);
+    if (!g_finish.host.load()) {
+        void *p = nullptr;
+        if (hipHostMalloc(&p, kFinishSlots * kFinishSlotStride * sizeof(uint64_t),
+                          hipHostMallocMapped | hipHostMallocPortable) != hipSuccess) {
+            (void)hipGetLastError();
+            return;
+        }
+        std::memset(p, 0, kFinishSlots * kFinishSlotStride * sizeof(uint64_t));
+        g_finish.host.store(static_cast<uint64_t *>(p));
+    }
+    if (!g_finish.dev[device].load()) {
+        void *d = nullptr;
+        if (hipHostGetDevicePointer(&d, g_finish.host.load(), 0) == hipSuccess)
+            g_finish.dev[device].store(static_cast<uint64_t *>(d));
+        else
+            (void)hipGetLastError();
+    }
+}
+
+// Waits until the work enqueued on `stream` so far has completed: through
+// a completion slot when the device has them (a signal kernel behind the
+// work, the host reading the slot without calling the runtime), else, or
+// after kFinishSpinUs, through hipStreamSynchronize.
+int wait_stream(int device, hipStream_t stream)
+{
+    uint64_t *dev_slots = (device >= 0 && device < kMaxDevices) ? g_finish.dev[device].load() : nullptr;
+    if (dev_slots) {
+        const uint64_t ticket = g_finish.next.fetch_add(1, std::memory_order_relaxed);
+        const uint64_t slot = (ticket % kFinishSlots) * kFinishSlotStride;
+        uint64_t *dp = dev_slots + slot;
+        void *args[] = {&dp, const_cast<uint64_t *>(&ticket)};
+        hipError_t e = hipLaunchKernel(reinterpret_cast<const void *>(&signal_host), dim3(1), dim3(64), args, 0,
+                                       stream);
+        if (e != hipSuccess)
+            return hip_error(e);
+        const uint64_t *hp = g_finish.host.load() + slot;
+        const auto t0 = std::chrono::steady_clock::now();
+        for (uint32_t k = 1;; ++k) {
+            if (__atomic_load_n(hp, __ATOMIC_ACQUIRE) >= ticket)
+                return LLMIG_OK;
+            if ((k & 1023u) == 0 &&
+                std::chrono::duration<double, std::micro>(std::chrono::steady_clock::now() - t0).count() >
+                    kFinishSpinUs)
+                break;
+        }
+    }
+    const hipError_t e = hipStreamSynchronize(stream);
+    return e == hipSuccess ? LLMIG_OK : hip_error(e);
 }
 
 bool same_geometry(const llmig_pool *a, const llmig_pool *b)
@@ -477,6 +565,7 @@ int llmig_pool_create(const llmig_pool_desc *desc, llmig_pool **out)
         // reported by that entry point, which looks it up again.
         void *unused = nullptr;
         (void)scratch_pointer(pool->device, &unused);
+        finish_slots_setup(pool->device);
         *out = pool.release();
         return LLMIG_OK;
     });
@@ -655,6 +744,17 @@ int llmig_migration_stage(llmig_migration *m, const llmig_pool *src, const llmig
         return launch_stage(src, dst, m->plan_src.data(), m->plan_dst.data(), n, false,
                             static_cast<hipStream_t>(stream), final_stage ? 0u : m->max_workgroups, ev);
     });
+}
+
+int llmig_migration_finish(llmig_migration *m, const llmig_pool *src, const llmig_pool *dst,
+                           const int32_t *src_table, int64_t src_table_len, int64_t len,
+                           const int32_t *dst_free_list, int64_t dst_free_len, void *stream, int64_t *out_n)
+{
+    int rc = llmig_migration_stage(m, src, dst, src_table, src_table_len, len, 1, dst_free_list, dst_free_len,
+                                   stream, out_n);
+    if (rc != LLMIG_OK)
+        return rc;
+    return no_throw([&]() -> int { return wait_stream(src->device, static_cast<hipStream_t>(stream)); });
 }
 
 int llmig_migration_set_stage_events(llmig_migration *m, void *start_event, void *stop_event)

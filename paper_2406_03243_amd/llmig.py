@@ -88,6 +88,9 @@ _lib.llmig_migration_next.restype = ctypes.c_int
 _lib.llmig_migration_stage.argtypes = [_vp, _vp, _vp, _vp, ctypes.c_int64, ctypes.c_int64, ctypes.c_int, _vp,
                                        ctypes.c_int64, _vp, _i64p]
 _lib.llmig_migration_stage.restype = ctypes.c_int
+_lib.llmig_migration_finish.argtypes = [_vp, _vp, _vp, _vp, ctypes.c_int64, ctypes.c_int64, _vp, ctypes.c_int64,
+                                        _vp, _i64p]
+_lib.llmig_migration_finish.restype = ctypes.c_int
 for _name in ("llmig_migration_abort", "llmig_migration_commit"):
     getattr(_lib, _name).argtypes = [_vp, _vp, ctypes.c_int64, _i64p]
     getattr(_lib, _name).restype = ctypes.c_int
@@ -286,6 +289,8 @@ class MigrationHandle:
         self._h = h
         self.block_size = int(block_size)
         self._copied = ctypes.c_int64(0)
+        self._n = ctypes.c_int64(0)
+        self._n_ref = ctypes.byref(self._n)
 
     def close(self):
         if getattr(self, "_h", None) is not None and _lib is not None:
@@ -333,6 +338,31 @@ class MigrationHandle:
                                          fl.ctypes.data, fl.size, out_s.ctypes.data, out_d.ctypes.data, cap,
                                          ctypes.byref(n)), "llmig_migration_next")
         return out_s[:n.value].copy(), out_d[:n.value].copy()
+
+    def stage_ptrs(self, src_handle, dst_handle, table_ptr: int, table_len: int, length: int, final: bool,
+                   free_ptr: int, free_len: int, stream_ptr: int) -> int:
+        """stage() with every argument already an address or an int (the
+        caller keeps the arrays alive): marshalling without conversions, for
+        drivers that call it on the downtime path."""
+        code = _lib.llmig_migration_stage(self._h, src_handle, dst_handle, table_ptr, table_len, length,
+                                          1 if final else 0, free_ptr, free_len, stream_ptr, self._n_ref)
+        if code != LLMIG_OK:
+            err = LlmigError(code, "llmig_migration_stage")
+            err.consumed = self._n.value
+            raise err
+        return self._n.value
+
+    def finish_ptrs(self, src_handle, dst_handle, table_ptr: int, table_len: int, length: int, free_ptr: int,
+                    free_len: int, stream_ptr: int) -> int:
+        """The final stage and the wait for it (llmig_migration_finish),
+        arguments as for stage_ptrs; returns the free-list entries consumed."""
+        code = _lib.llmig_migration_finish(self._h, src_handle, dst_handle, table_ptr, table_len, length, free_ptr,
+                                           free_len, stream_ptr, self._n_ref)
+        if code != LLMIG_OK:
+            err = LlmigError(code, "llmig_migration_finish")
+            err.consumed = self._n.value
+            raise err
+        return self._n.value
 
     def stage(self, src: "Pool", dst: "Pool", src_table: np.ndarray, length: int, final: bool,
               dst_free_list: np.ndarray, stream=None) -> int:

@@ -65,11 +65,19 @@ class Migration:
         self._free0 = np.ascontiguousarray(np.asarray(dst_free_list, dtype=np.int32))
         self._consumed = 0
         self.copied_tok = 0
+        self.finished_at = None
         self.stages: list[StageRecord] = []
         self._events = []
         self.coord = MigrationHandle(self.bs)
         if max_workgroups:
             self.coord.set_max_workgroups(max_workgroups)
+        # addresses for the stage calls, taken once (the arrays live as long
+        # as the migration): the final stage's call is on the downtime path
+        self._table_ptr = self.src_table.ctypes.data
+        self._free_ptr = self._free0.ctypes.data
+        if src is not None:
+            self._handles = (src.handle, dst.handle)
+            self._stream_ptr = stream.cuda_stream
 
     @property
     def free(self) -> np.ndarray:
@@ -107,7 +115,9 @@ class Migration:
             ev = _timer_pair()
             self.coord.set_stage_events(*ev)
         try:
-            n = self.coord.stage(self.src, self.dst, self.src_table, length, final, self.free, stream=self.stream)
+            n = self.coord.stage_ptrs(*self._handles, self._table_ptr, self.src_table.size, length, final,
+                                      self._free_ptr + 4 * self._consumed, self._free0.size - self._consumed,
+                                      self._stream_ptr)
         except LlmigError as e:
             self._consumed += getattr(e, "consumed", 0)   # reserved before a HIP failure: abort returns them
             raise
@@ -115,6 +125,29 @@ class Migration:
             _spare_timers.append(ev)    # not recorded by the library: free again
             ev = None
         return self._record(length, n, final, ev)
+
+    def finish(self, length: int, time_it: bool = False) -> StageRecord:
+        """The final stage for a drained request now holding ``length``
+        tokens, returning once its copy is complete (one library call that
+        launches and waits, so no host work sits between the two).
+        ``finished_at`` is the perf_counter time at which the call returned;
+        the bookkeeping after it is not downtime."""
+        ev = None
+        if time_it:
+            ev = _timer_pair()
+            self.coord.set_stage_events(*ev)
+        try:
+            n = self.coord.finish_ptrs(*self._handles, self._table_ptr, self.src_table.size, length,
+                                       self._free_ptr + 4 * self._consumed, self._free0.size - self._consumed,
+                                       self._stream_ptr)
+            self.finished_at = time.perf_counter()   # the host has seen the copy complete
+        except LlmigError as e:
+            self._consumed += getattr(e, "consumed", 0)
+            raise
+        if time_it and n == 0:
+            _spare_timers.append(ev)
+            ev = None
+        return self._record(length, n, True, ev)
 
     def plan(self, length: int, final: bool):
         """The same step without the copy (host only): reserve and plan the
@@ -170,9 +203,8 @@ def run_scheduled(src: Pool, dst: Pool, src_table, dst_free_list, initial_len: i
             mig_stream.synchronize()
             ev.synchronize()
             t0 = time.perf_counter()
-            m.stage(length, final=True, time_it=time_final)
-            mig_stream.synchronize()
-            downtime_us = (time.perf_counter() - t0) * 1e6
+            m.finish(length, time_it=time_final)
+            downtime_us = (m.finished_at - t0) * 1e6
         else:
             mig_stream.wait_event(ev)
             m.stage(length, final=False, time_it=time_all)
@@ -219,9 +251,8 @@ def run_timed(src: Pool, dst: Pool, src_table, initial_len: int, dst_free_list, 
         if m.remaining_blocks(length) <= last_stage_max_blocks or len(m.stages) + 1 >= max_stages:
             ev.synchronize()
             t0 = time.perf_counter()
-            m.stage(length, final=True, time_it=time_final)
-            mig_stream.synchronize()
-            downtime_us = (time.perf_counter() - t0) * 1e6
+            m.finish(length, time_it=time_final)
+            downtime_us = (m.finished_at - t0) * 1e6
             break
         mig_stream.wait_event(ev)
         rec = m.stage(length, final=False)

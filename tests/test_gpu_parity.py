@@ -338,6 +338,38 @@ def test_coordinator_commit_table():
     assert oracle.default().first_token_mismatch(host_image(src), table, host_image(dst), got, 233) == -1
 
 
+def test_coordinator_finish_waits_and_refuses():
+    """llmig_migration_finish: the final stage returns with its copy done
+    (the destination is read back with no further synchronisation of the
+    migration stream); a free list too short for it is refused before
+    anything is reserved or enqueued, and a later finish with room works."""
+    shape = wl.PoolShape(2, 150, 16, 4, 64, "fp16")
+    say("coordinator finish", shape)
+    src = make_pool(shape, 91, wl.SRC_VALUES)
+    dst = make_pool(shape, 91, wl.DST_VALUES)
+    table, _ = wl.request_table(91, shape.num_blocks, 40)
+    free, _ = wl.free_list(91, shape.num_blocks)
+    hs, hd = host_image(src), host_image(dst)
+    mig = torch.cuda.Stream()
+    m = migrate.Migration(src, dst, table, free, mig)
+    m.stage(320, final=False)              # 20 blocks
+    mig.synchronize()
+    short = migrate.Migration(src, dst, table, free, mig)
+    short.stage(320, final=False)
+    mig.synchronize()
+    short._free0 = short._free0[:22].copy()    # 2 entries left: the final stage needs 3
+    short._free_ptr = short._free0.ctypes.data
+    with pytest.raises(LlmigError) as e:
+        short.finish(355)
+    assert e.value.name == "ENOSPC" and short.coord.info()["reserved_blocks"] == 20
+    rec = m.finish(355)                    # 20 -> 23 blocks, the last one partial
+    assert rec.final and rec.from_tok == 320 and rec.to_tok == 355 and rec.blocks == 3
+    got = m.commit()
+    oracle.default().copy(hs, hd, table[:23], got)
+    assert_same(host_image(dst), hd, "destination after finish")
+    assert oracle.default().first_token_mismatch(hs, table, host_image(dst), got, 355) == -1
+
+
 @pytest.mark.parametrize("cap", [1, 7, 64])
 def test_capped_grid_multistage(cap):
     """Throttled migrations: a capped grid walks many items per workgroup."""
@@ -412,6 +444,57 @@ def test_concurrent_stages_from_threads():
                 orc.copy_layout(hs, (0, 0), want, layouts[j], ms, md, 4, 64, 2)
         assert_same(host_image(d), want, f"destination {j}")
     assert_same(host_image(src), hs, "source")
+
+
+def test_concurrent_finishes_from_threads():
+    """Eight host threads each run whole migrations (a first stage, then
+    llmig_migration_finish) from one shared source pool into destination
+    pools of their own, on their own streams, twenty times over: the
+    completion tickets of concurrent final stages never cross (each
+    finish returns only after its own copy, checked by reading the
+    destination right away), and the results match the oracle."""
+    import threading
+    say("concurrent finishes, 8 threads x 20")
+    shape = wl.PoolShape(2, 300, 16, 4, 64, "fp16")
+    seed = 9200
+    src = make_pool(shape, seed, wl.SRC_VALUES, random_bytes=True)
+    hs = host_image(src)
+    n_threads, rounds = 8, 20
+    dsts = [make_pool(shape, seed + 1 + j, wl.DST_VALUES) for j in range(n_threads)]
+    table, _ = wl.request_table(seed, shape.num_blocks, 40)
+    errors, results = [], {}
+
+    def worker(j):
+        try:
+            st = torch.cuda.Stream()
+            g = wl.stream(seed, wl.EXTRA, j)
+            for r in range(rounds):
+                free = g.permutation(shape.num_blocks).astype(np.int32)
+                length = int(g.integers(17, 600))
+                m = migrate.Migration(src, dsts[j], table, free, st)
+                m.stage(length, final=False, time_it=False)
+                m.finish(length)
+                got = m.commit()
+                # no synchronisation here: finish has already waited for the copy
+                snap = [harness.tile_view(t).index_select(0, torch.as_tensor(got.astype(np.int64), device="cuda"))
+                        .cpu().numpy() for t in dsts[j].k + dsts[j].v]
+                results[(j, r)] = (length, got, snap)
+        except Exception as e:          # reported below, on the main thread
+            errors.append((j, e))
+
+    threads = [threading.Thread(target=worker, args=(j,)) for j in range(n_threads)]
+    for t in threads:
+        t.start()
+    for t in threads:
+        t.join()
+    torch.cuda.synchronize()
+    assert not errors, errors
+    for (j, r), (length, got, snap) in results.items():
+        nb = len(got)
+        assert nb == -(-length // shape.block_size)
+        for l in range(shape.num_layers):
+            for kv, a in enumerate((hs.k[l], hs.v[l])):
+                assert np.array_equal(snap[kv * shape.num_layers + l], a[table[:nb]]), (j, r, l, kv)
 
 
 def test_stage_events_bracket_the_kernels():
