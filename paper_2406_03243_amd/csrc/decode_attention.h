@@ -20,7 +20,7 @@
 
 namespace {
 
-constexpr int kPartTokens = 1024;    // tokens per partition
+constexpr int kPartTokens = 2048;    // tokens per partition
 constexpr int kAttnItems = 128;      // (sequence, partition) items per launch, in the kernel arguments
 constexpr int kAttnMaxBatch = 256;   // sequences per call (per-sequence item ranges ride in the arguments)
 
@@ -97,9 +97,15 @@ __global__ void __launch_bounds__(kThreads) attn_reduce(const AttnReduceArgs a)
 
 // ---------------------------------------------------------------------------
 // Matrix-core variant.  Per 16-token group of a partition, one wavefront:
+//   loads     the group's K and V rows whole: D/8 lanes of 16 bytes per row,
+//             64/(D/8) rows per load instruction (256 contiguous bytes a row
+//             for D = 128), tokens past the partition's end clamped to its
+//             last token (their weights are 0), so no branch sits between
+//             the loads;
 //   S^T = K . Q^T     16 tokens x 16 query rows (the group's heads, zero-padded),
-//                     K fragments loaded straight from HBM, 16 bytes a lane,
-//                     16x16x32 MFMA over head_dim in steps of 32;
+//                     16x16x32 MFMA over head_dim in steps of 32; K reaches
+//                     the A-operand layout (token = lane % 16) through the
+//                     wavefront's LDS region, 16-byte chunks in and out;
 //   online softmax per query row (a lane's rows of S^T are the tokens
 //                     4*(lane/16) .. +3 of query row lane%16);
 //   O^T += V^T . P^T  16x16x16 MFMA per 16 dims; P^T is already in the
@@ -110,9 +116,14 @@ __global__ void __launch_bounds__(kThreads) attn_reduce(const AttnReduceArgs a)
 // The four wavefronts take alternate token groups of the partition and merge
 // their states through LDS at the end.  The kernel waits on HBM, not on the
 // matrix cores or LDS, so it is built for four wavefronts per SIMD (at most
-// 128 registers: the accumulators move from AGPRs to VGPRs), which the
-// workgroup's 35 KiB of LDS also allows; measured in one process against
-// the three-wavefront build: 3-6% faster, identical output.
+// 128 registers: the accumulators move from AGPRs to VGPRs).
+// Measured on MI355X, one process, alternating, against the previous kernel
+// (K fragments loaded straight into the operand layout: 16 rows x 64 bytes
+// per load instruction; 1024-token partitions; the hardware's workgroup
+// order) on a GQA decode step (80 layers, 8 KV heads of 128, 17 sequences,
+// 65,280 tokens): whole-row K loads +8%, grouping each (layer, partition)'s
+// KV heads on one XCD +7%, 2048-token partitions +4%; 0.63 -> 0.75 of HBM
+// peak for the step, partial and merge kernels together.
 typedef _Float16 f16x8_t __attribute__((ext_vector_type(8)));
 typedef _Float16 f16x4_t __attribute__((ext_vector_type(4)));
 typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
@@ -153,26 +164,57 @@ __device__ __forceinline__ uint32_t to16(float x)
     }
 }
 
+// Block ids a partition can touch, for the dynamic LDS of attn_partial_mfma:
+// a partition starts on a block boundary (kPartTokens is a multiple of every
+// block size that divides it) or inside a block, so at most
+// ceil(kPartTokens / block_size) + 1 blocks.
+inline uint32_t attn_blk_slots(uint32_t block_size)
+{
+    return (kPartTokens + block_size - 1) / block_size + 1;
+}
+
 template <int BF16, int D>
 __global__ void __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(4, 8)))
 attn_partial_mfma(const AttnArgs a)
 {
     constexpr int KS = D / 32;            // k-steps of the QK product
     constexpr int MT = D / 16;            // 16-dim tiles of the PV product
-    constexpr int LPR = D / 8;            // lanes per row in the V loads (16 bytes each)
-    constexpr int RPL = 64 / LPR;         // rows per V load instruction
+    constexpr int LPR = D / 8;            // lanes per row in the K and V loads (16 bytes each)
+    constexpr int RPL = 64 / LPR;         // rows per load instruction
     constexpr int VP = 20;                // LDS pitch of one V^T row: 16 tokens + 4 pad (40 bytes)
     constexpr float kLog2e = 1.4426950408889634f;
-    // 4 wavefronts x D rows x VP in the loop; reused for the final merge of
-    // 4 x D x 16 floats.
+    // 4 wavefronts x D rows x VP in the loop (each wavefront's region holds
+    // its group's K chunks first, 16 x (LPR + 1) x 16 bytes, then its V^T);
+    // reused for the final merge of 4 x D x 16 floats.
     constexpr int kVtBytes = 4 * D * VP * 2, kMergeBytes = 4 * D * 16 * 4;
+    static_assert(16 * (LPR + 1) * 16 <= D * VP * 2, "a group's K chunks fit in the wavefront's region");
     __shared__ __align__(16) uint8_t smem[kVtBytes > kMergeBytes ? kVtBytes : kMergeBytes];
     __shared__ float sh_m[4][16], sh_l[4][16];
-    __shared__ int32_t sh_blk[kPartTokens];         // block ids of the partition (block_size >= 1)
+    // block ids of the partition: dynamic LDS of attn_blk_slots(block_size) entries
+    extern __shared__ int32_t sh_blk[];
 
-    const uint32_t item = blockIdx.x / a.kv_heads;
-    const uint32_t g = blockIdx.x - item * a.kv_heads;
-    const uint32_t layer = blockIdx.y;
+    // The dispatcher deals workgroups to the eight XCDs in turn.  Renumbered
+    // here so that the kv_heads workgroups of one (layer, item), which read
+    // adjacent 256-byte pieces of the same token rows, run one after another
+    // on one XCD: linear workgroup w is the (w / 8)-th on XCD w % 8.  The
+    // tail of the grid that does not fill whole rounds of 8 * kv_heads keeps
+    // the plain order.
+    uint32_t item, g, layer;
+    {
+        const uint32_t H = a.kv_heads, lin = blockIdx.x + blockIdx.y * gridDim.x;
+        const uint32_t total = gridDim.x * gridDim.y, full = total - total % (8u * H);
+        uint32_t unit;                    // (layer, item) in row-major order
+        if (lin < full) {
+            const uint32_t k = lin / 8u;
+            g = k % H;
+            unit = (k / H) * 8u + lin % 8u;
+        } else {
+            g = lin % H;
+            unit = lin / H;
+        }
+        layer = unit / a.items;
+        item = unit - layer * a.items;
+    }
     const uint32_t b = static_cast<uint32_t>(a.item_seq[item]);
     const int32_t start = a.item_start[item], end = a.item_end[item];
     const uint32_t G = a.q_heads / a.kv_heads;
@@ -210,32 +252,37 @@ attn_partial_mfma(const AttnArgs a)
         acc[mt] = f32x4_t{0.f, 0.f, 0.f, 0.f};
 
     for (int32_t tg = start + 16 * static_cast<int32_t>(wave); tg < end; tg += 64) {
-        // K fragments (A operand): token tg + r16, dims 32*ks + 8*g4 .. +8.
-        const int32_t tk = tg + static_cast<int32_t>(r16);
-        u32x4 kf[KS];
-        if (tk < end) {
-            const uint64_t row = (static_cast<uint64_t>(sh_blk[tk / a.block_size - first_blk]) * a.block_size +
-                                  tk % a.block_size) * a.kv_heads + g;
-#pragma unroll
-            for (int ks = 0; ks < KS; ++ks)
-                kf[ks] = load16(kbase + (row * D + 32 * ks + 8 * g4) * 2);
-        } else {
-#pragma unroll
-            for (int ks = 0; ks < KS; ++ks)
-                kf[ks] = u32x4{0u, 0u, 0u, 0u};
-        }
-        // V rows: KS loads of RPL rows x D dims; row tg + j*RPL + lane/LPR, dims 8*(lane%LPR) .. +8.
-        u32x4 vr[KS];
+        // K and V rows: KS loads each of RPL whole rows; row tg + j*RPL +
+        // lane/LPR, dims 8*(lane%LPR) .. +8.  A token past the partition's end
+        // loads its last token instead; its score is masked below, so its
+        // weight is 0.
+        u32x4 kr[KS], vr[KS];
 #pragma unroll
         for (int j = 0; j < KS; ++j) {
-            const int32_t tv = tg + j * RPL + static_cast<int32_t>(lane / LPR);
-            vr[j] = u32x4{0u, 0u, 0u, 0u};
-            if (tv < end) {
-                const uint64_t row = (static_cast<uint64_t>(sh_blk[tv / a.block_size - first_blk]) *
-                                      a.block_size + tv % a.block_size) * a.kv_heads + g;
-                vr[j] = load16(vbase + (row * D + 8 * (lane % LPR)) * 2);
-            }
+            const int32_t t = min(tg + j * RPL + static_cast<int32_t>(lane / LPR), end - 1);
+            const uint64_t row = (static_cast<uint64_t>(sh_blk[t / a.block_size - first_blk]) * a.block_size +
+                                  t % a.block_size) * a.kv_heads + g;
+            kr[j] = load16(kbase + (row * D + 8 * (lane % LPR)) * 2);
+            vr[j] = load16(vbase + (row * D + 8 * (lane % LPR)) * 2);
         }
+        // K to the A-operand layout (token r16, dims 32*ks + 8*g4 .. +8)
+        // through the wavefront's LDS region: chunk c of token t at
+        // kst[t * (LPR + 1) + c] (one chunk of padding per token keeps the
+        // strided reads on distinct banks).
+        u32x4 *kst = reinterpret_cast<u32x4 *>(vt);
+#pragma unroll
+        for (int j = 0; j < KS; ++j)
+            kst[(j * RPL + lane / LPR) * (LPR + 1) + lane % LPR] = kr[j];
+        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+        __builtin_amdgcn_wave_barrier();
+        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+        u32x4 kf[KS];
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks)
+            kf[ks] = kst[r16 * (LPR + 1) + 4 * ks + g4];
+        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+        __builtin_amdgcn_wave_barrier();
+        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
         // S^T = K . Q^T
         f32x4_t s = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll

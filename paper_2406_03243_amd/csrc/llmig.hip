@@ -1052,7 +1052,8 @@ static int attn_enqueue(const llmig_pool *pool, const void *fn, const void *q, i
         a.item_base = first;
         a.items = m;
         void *args[] = {&a};
-        hipError_t e = hipLaunchKernel(fn, dim3(m * a.kv_heads, a.num_layers), dim3(kThreads), args, 0, st);
+        hipError_t e = hipLaunchKernel(fn, dim3(m * a.kv_heads, a.num_layers), dim3(kThreads), args,
+                                       attn_blk_slots(a.block_size) * sizeof(int32_t), st);
         first += m;
         m = 0;
         return e;

@@ -3,7 +3,7 @@
 The GPU parity test accepts the kernel's output when it lies within the
 bound of tests/attn_cases.py of the fp64 oracle.  A bound that grows with
 the sequence length alone would also accept an output that lost a whole
-1024-token partition of a long sequence, or the partitions of the second
+2048-token partition of a long sequence, or the partitions of the second
 launch of a call, which is exactly the kind of mistake a flash-decoding
 merge can make.  Here, for every fixed case, the oracle's own result with
 such a piece dropped must violate the bound, while the exact result passes
@@ -33,7 +33,9 @@ def _dropped(orc, case, host, q, tables, ctx, scale, pieces):
     return orc.decode_attention(host, kv_heads, head_dim, dtype, q, t, n, scale)
 
 
-MULTI = [c for c in ac.CASES if max(c[6]) > ac.PART_TOKENS]
+# cases with a sequence of several partitions (the two-launch case, whose
+# oracle calls take seconds each, is the second test's)
+MULTI = [c for c in ac.CASES if ac.PART_TOKENS < max(c[6]) <= 50000]
 
 
 @pytest.mark.parametrize("case", MULTI, ids=ac.case_id)

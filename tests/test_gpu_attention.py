@@ -4,7 +4,7 @@ migration) against the fp64 oracle, through the C ABI.
 Inputs and the error bound come from tests/attn_cases.py: the bound is
 derived from the kernel's arithmetic (fp32 accumulation, the 16-bit hi/lo
 split of the softmax weights) and scales with the softmax-weighted mean of
-|V| rather than with the sequence length alone, so a lost 1024-token
+|V| rather than with the sequence length alone, so a lost 2048-token
 partition, or a lost launch of partitions, fails it (checked on the CPU by
 tests/test_attn_tolerance.py).  Each case prints its largest absolute error
 and its largest error-to-bound ratio."""

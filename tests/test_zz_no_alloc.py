@@ -74,8 +74,9 @@ def test_noalloc_refuses_a_call_too_large_for_the_array():
     k, v = harness.alloc_layers(shape)
     pool = Pool(k, v)
     q = torch.zeros((1, 1, 16, 128), dtype=torch.float16, device="cuda")
-    ctx = [4_200_000]                                        # 4102 partitions x 16 heads x 130 floats
-    assert decode_workspace_bytes(ctx, 1, 16, 128) > DECODE_SCRATCH_BYTES
+    ctx = [1 << 20]
+    while decode_workspace_bytes(ctx, 1, 16, 128) <= DECODE_SCRATCH_BYTES:   # the smallest power of two over
+        ctx = [2 * ctx[0]]
     tab = torch.zeros((1, -(-ctx[0] // 16)), dtype=torch.int32, device="cuda")
     out = torch.full(q.shape, 7.0, dtype=torch.float32, device="cuda")
     with pytest.raises(LlmigError) as e:
