@@ -381,14 +381,19 @@ def cpu_baseline(src, ids, shape, what):
     threads = max(1, min(CPU_SHARE, affinity, n))
     single = leg(1)
     multi = leg(threads)
-    model = ""
+    # the host CPU as the kernel reports it (a virtual machine may report
+    # only the brand): name, family/model/stepping and clock of the first CPU
+    info = {}
     try:
         for line in open("/proc/cpuinfo"):
-            if line.startswith("model name"):
-                model = line.split(":", 1)[1].strip()
+            if not line.strip():
                 break
+            key, _, val = line.partition(":")
+            info[key.strip()] = val.strip()
     except OSError:
         pass
+    model = info.get("model name", "")
+    ident = {k.replace(" ", "_"): info[k] for k in ("cpu family", "model", "stepping", "cpu MHz") if k in info}
     return {"value": multi["value"], "unit": "GB/s", "cores": threads, "kind": "oracle",
             "sample": f"{what}: all {shape.num_layers} layers, K and V, {n * shape.num_layers * 2} tiles of "
                       f"{src.tile_bytes} B, copied from host snapshots (a compact pool of the mapped blocks) by "
@@ -396,7 +401,7 @@ def cpu_baseline(src, ids, shape, what):
                       f"warm-ups per leg",
             "all_cores": multi, "single_thread": single,
             "affinity_cpus": affinity, "nproc": os.cpu_count(), "cpu_share_cap": CPU_SHARE,
-            "cpu_model": model}
+            "cpu_model": model, "cpu_id": ident}
 
 
 def downtime_sweep(reps):

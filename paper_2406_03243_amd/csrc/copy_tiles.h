@@ -27,9 +27,11 @@
 //    zeros for its load and drops its store.  Predicating those rows on
 //    the lane mask instead makes the compiler wait for every earlier memory
 //    operation before each store of the span (it cannot count them across
-//    the branches), which serialised the tail's stores: 52 KiB tiles moved
-//    at 0.62-0.67 of HBM peak that way and at 0.72-0.75 this way, in one
-//    process, alternating (128 and 32 KiB tiles gained about 1%).
+//    the branches), which serialised the tail's stores.  Measured on 52 KiB
+//    tiles in one process, alternating: predicated rows 0.62 of HBM peak; a
+//    separate, range-checked code path for short spans only 0.67-0.68; one
+//    sequence for every span 0.72-0.75 (128 and 32 KiB tiles gained about
+//    1%).
 //  * Wave items run pair-major (all spans of all layers of one block pair,
 //    then the next pair); one workgroup per four items unless the grid is
 //    capped, in which case resident workgroups walk the items.

@@ -6,10 +6,10 @@ blocks a migration touches, snapshotted before it starts, behind an id remap
 (request block j -> compact id j, consumed destination block k -> compact id
 k).  The LLaMA-7B migration, the LLaMA-30B quarter at 1k, 4k and 16k tokens,
 the GQA migration and the cross-layout LLaMA-7B stage (converted element by
-element by the oracle) are replayed block for block; the batched workload
-(2,642 pairs) is replayed on a sample of pairs, with every pair checked on
-the device for equality of source and destination tiles (a property that
-holds at any size).  Tolerance 0."""
+element by the oracle) are replayed block for block; so is the batched
+workload (2,642 pairs, 44 GB read and written), in chunks of 256 pairs,
+its mapping planned request by request by the oracle's planner.  Tolerance
+0."""
 import sys
 
 import numpy as np
@@ -62,6 +62,43 @@ def device_pairs_equal(src, dst, ms, md) -> bool:
         if not torch.equal(harness.tile_view(a).index_select(0, si), harness.tile_view(b).index_select(0, di)):
             return False
     return True
+
+
+def oracle_batch_plan(tables, lengths, free, block_size):
+    """The batched stage's pairs as the oracle plans them: each request's
+    whole length, destination blocks from the head of what the requests
+    before it left of the free list."""
+    orc, rest, ms, md = oracle.default(), np.asarray(free, np.int32), [], []
+    for table, length in zip(tables, lengths):
+        code, s, d = orc.plan(table, rest, int(length), 0, int(length), block_size)
+        assert code == oracle.OK
+        ms.append(s)
+        md.append(d)
+        rest = rest[len(d):]
+    return np.concatenate(ms), np.concatenate(md)
+
+
+CHUNK_PAIRS = 256
+
+
+def snapshot_chunks(pool, ids):
+    return [compact(pool, ids[lo:lo + CHUNK_PAIRS]) for lo in range(0, len(ids), CHUNK_PAIRS)]
+
+
+def replay_every_pair(src, dst, ms, md, before):
+    """Every pair through the oracle: the source blocks as they were before
+    the migration (``before``, chunks of CHUNK_PAIRS pairs) copied by the
+    oracle into zeroed compact blocks and compared with the device's
+    destination blocks; the source blocks are still what they were."""
+    orc = oracle.default()
+    for c, hs in enumerate(before):
+        lo = c * CHUNK_PAIRS
+        n = hs.num_blocks
+        hd = HostPool.zeros(hs.num_layers, n, src.block_size, src.slot_bytes)
+        ids = np.arange(n, dtype=np.int32)
+        orc.copy(hs, hd, ids, ids)
+        assert_same(compact(dst, md[lo:lo + n]), hd, f"destination blocks of pairs {lo}..{lo + n - 1}")
+        assert_same(compact(src, ms[lo:lo + n]), hs, f"source blocks of pairs {lo}..{lo + n - 1}")
 
 
 def untouched_sample(dst, mapped, k, seed):
@@ -148,18 +185,16 @@ def test_batched_one_call_full():
     say("batched full", su.shape, len(su.tables))
     ms, md, per_req = migrate.plan_batch(su.tables, su.lengths, su.free, su.shape.block_size)
     assert len(ms) == sum(-(-n // su.shape.block_size) for n in su.lengths)
-    sample = np.sort(wl.stream(su.workload.seed, wl.EXTRA, 3).choice(len(ms), 256, replace=False))
-    hs = compact(su.src, ms[sample])
-    hd = compact(su.dst, md[sample])
+    oms, omd = oracle_batch_plan(su.tables, su.lengths, su.free, su.shape.block_size)
+    assert np.array_equal(ms, oms) and np.array_equal(md, omd)
+    before = snapshot_chunks(su.src, oms)
     guard = untouched_sample(su.dst, md, 256, 2)
     guard_before = compact(su.dst, guard)
     src_occ = su.src_occupied[:256]
     src_occ_before = compact(su.src, src_occ)
     llmig_stage(su.src, su.dst, ms, md)
     torch.cuda.synchronize()
-    ids = np.arange(len(sample), dtype=np.int32)
-    oracle.default().copy(hs, hd, ids, ids)
-    assert_same(compact(su.dst, md[sample]), hd, "sampled destination blocks")
+    replay_every_pair(su.src, su.dst, oms, omd, before)
     assert device_pairs_equal(su.src, su.dst, ms, md)
     assert_same(compact(su.dst, guard), guard_before, "destination blocks outside the mapping")
     assert_same(compact(su.src, src_occ), src_occ_before, "source blocks of other requests")
@@ -171,9 +206,9 @@ def test_batched_host_staged_full(mode):
     su = scenarios.batched()
     say("batched host staged", mode, su.shape)
     ms, md, _ = migrate.plan_batch(su.tables, su.lengths, su.free, su.shape.block_size)
-    sample = np.sort(wl.stream(su.workload.seed, wl.EXTRA, 4).choice(len(ms), 128, replace=False))
-    hs = compact(su.src, ms[sample])
-    hd = compact(su.dst, md[sample])
+    oms, omd = oracle_batch_plan(su.tables, su.lengths, su.free, su.shape.block_size)
+    assert np.array_equal(ms, oms) and np.array_equal(md, omd)
+    before = snapshot_chunks(su.src, oms)
     guard = untouched_sample(su.dst, md, 128, 3)
     guard_before = compact(su.dst, guard)
     chunk = 64
@@ -186,9 +221,7 @@ def test_batched_host_staged_full(mode):
     migrate.run_host_staged(su.src, su.dst, ms, md, bufs, *harness.concurrent_streams(2)[0], chunk,
                             dev_bufs=dev_bufs)
     torch.cuda.synchronize()
-    ids = np.arange(len(sample), dtype=np.int32)
-    oracle.default().copy(hs, hd, ids, ids)
-    assert_same(compact(su.dst, md[sample]), hd, "sampled destination blocks")
+    replay_every_pair(su.src, su.dst, oms, omd, before)
     assert device_pairs_equal(su.src, su.dst, ms, md)
     assert_same(compact(su.dst, guard), guard_before, "destination blocks outside the mapping")
     su.close()
