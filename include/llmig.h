@@ -363,9 +363,10 @@ int llmig_stream_read(const void *region, int64_t bytes, int32_t passes, int32_t
  * [num_layers][batch][q_heads][head_dim] of the pool's 16-bit type (dtype 0
  * fp16, 1 bf16), 16-byte aligned; tables device int32, ids the caller
  * guarantees in range; ctx_lens a HOST array; out device float32
- * [num_layers][batch][q_heads][head_dim]; a sequence of length 0 gives
- * zeros.  workspace: device memory of at least the size
- * llmig_decode_attention_workspace returns for the same lengths.
+ * [num_layers][batch][q_heads][head_dim], 16-byte aligned; a sequence of
+ * length 0 gives zeros.  workspace: device memory of at least the size
+ * llmig_decode_attention_workspace returns for the same lengths, 16-byte
+ * aligned.
  * Supported: NHD pools, head_dim 64 or 128, q_heads / num_kv_heads in
  * {1, 2, 4, 8, 16}, batch <= 256; else LLMIG_EINVAL.  Arithmetic in fp32. */
 int llmig_decode_attention_workspace(const int32_t *ctx_lens, int32_t batch, int32_t num_layers,

@@ -23,12 +23,16 @@ namespace {
 constexpr int kPartTokens = 2048;    // tokens per partition
 constexpr int kAttnItems = 128;      // (sequence, partition) items per launch, in the kernel arguments
 constexpr int kAttnMaxBatch = 256;   // sequences per call (per-sequence item ranges ride in the arguments)
+// A partial result record: the partition's maximum score m (natural base),
+// its weight sum l, two floats of padding, then the D weighted V sums, so
+// that records (D + kAttnHeader floats) and their sums start on 16 bytes.
+constexpr int kAttnHeader = 4;
 
 struct AttnArgs {
     const uint64_t *k_tab;      // pool tables: K bases then V bases
     const uint8_t *q;           // [L][B][Hq][D]
     const int32_t *tables;      // [B][table_stride]
-    float *ws;                  // partial results: [L][n_items][Hq][D + 2]
+    float *ws;                  // partial results: [L][n_items][Hq][D + kAttnHeader]
     float scale;
     uint32_t num_layers, batch, q_heads, kv_heads, block_size, table_stride;
     uint32_t item_base;         // global index of this launch's first item
@@ -47,51 +51,60 @@ struct AttnReduceArgs {
     int32_t seq_count[kAttnMaxBatch];   // its number of items (0 for an empty sequence)
 };
 
-// One lane per (layer, sequence, query head, dimension): merges the
-// partitions of the sequence and normalises.
+// One lane per (layer, sequence, query head, four dimensions): merges the
+// partitions of the sequence and normalises.  A lane reads each partition's
+// m and l as one 8-byte load and its four sums as one 16-byte load, eight
+// partitions at a time so their loads are in flight together; the
+// head_dim / 4 lanes of one (layer, sequence, query head) read one record's
+// sums whole.
 __global__ void __launch_bounds__(kThreads) attn_reduce(const AttnReduceArgs a)
 {
-    const uint64_t total = static_cast<uint64_t>(a.num_layers) * a.batch * a.q_heads * a.head_dim;
+    const uint32_t quads = a.head_dim / 4;
+    const uint32_t rec = a.head_dim + kAttnHeader;                       // floats per record
+    const uint64_t total = static_cast<uint64_t>(a.num_layers) * a.batch * a.q_heads * quads;
     for (uint64_t x = static_cast<uint64_t>(blockIdx.x) * kThreads + threadIdx.x; x < total;
          x += static_cast<uint64_t>(gridDim.x) * kThreads) {
-        const uint32_t d = x % a.head_dim;
-        uint64_t r = x / a.head_dim;
+        const uint32_t d4 = x % quads;
+        uint64_t r = x / quads;
         const uint32_t h = r % a.q_heads;
         r /= a.q_heads;
         const uint32_t b = r % a.batch;
         const uint32_t layer = static_cast<uint32_t>(r / a.batch);
-        float m = -INFINITY, l = 0.f, acc = 0.f;
+        float m = -INFINITY, l = 0.f;
+        float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
         const int32_t count = a.seq_count[b];
-        const uint64_t stride = static_cast<uint64_t>(a.q_heads) * (a.head_dim + 2); // one partition
+        const uint64_t stride = static_cast<uint64_t>(a.q_heads) * rec;  // one partition
         const float *base = a.ws + ((static_cast<uint64_t>(layer) * a.n_items_total + a.seq_first[b]) * a.q_heads + h) *
-                                       (a.head_dim + 2);
-        // partitions in batches of 8 so their loads are in flight together
+                                       rec;
         for (int32_t p0 = 0; p0 < count; p0 += 8) {
-            float m2[8], l2[8], a2[8];
+            float2 ml[8];
+            float4 v[8];
 #pragma unroll
             for (int u = 0; u < 8; ++u) {
-                m2[u] = -INFINITY;
-                l2[u] = 0.f;
-                a2[u] = 0.f;
+                ml[u] = make_float2(-INFINITY, 0.f);
+                v[u] = make_float4(0.f, 0.f, 0.f, 0.f);
                 if (p0 + u < count) {
                     const float *src = base + (p0 + u) * stride;
-                    m2[u] = src[0];
-                    l2[u] = src[1];
-                    a2[u] = src[2 + d];
+                    ml[u] = *reinterpret_cast<const float2 *>(src);
+                    v[u] = *reinterpret_cast<const float4 *>(src + kAttnHeader + 4 * d4);
                 }
             }
 #pragma unroll
             for (int u = 0; u < 8; ++u) {
-                const float mm = fmaxf(m, m2[u]);
+                const float mm = fmaxf(m, ml[u].x);
                 if (mm == -INFINITY)
                     continue;
-                const float c1 = __expf(m - mm), c2 = __expf(m2[u] - mm);
-                l = l * c1 + l2[u] * c2;
-                acc = acc * c1 + a2[u] * c2;
+                const float c1 = __expf(m - mm), c2 = __expf(ml[u].x - mm);
+                l = l * c1 + ml[u].y * c2;
+                acc.x = acc.x * c1 + v[u].x * c2;
+                acc.y = acc.y * c1 + v[u].y * c2;
+                acc.z = acc.z * c1 + v[u].z * c2;
+                acc.w = acc.w * c1 + v[u].w * c2;
                 m = mm;
             }
         }
-        a.out[x] = l > 0.f ? acc / l : 0.f;
+        reinterpret_cast<float4 *>(a.out)[x] =
+            l > 0.f ? make_float4(acc.x / l, acc.y / l, acc.z / l, acc.w / l) : make_float4(0.f, 0.f, 0.f, 0.f);
     }
 }
 
@@ -369,17 +382,19 @@ attn_partial_mfma(const AttnArgs a)
         }
         const uint64_t slot = (static_cast<uint64_t>(layer) * a.n_items_total + a.item_base + item) * a.q_heads +
                               g * G + r16;
-        float *dst = a.ws + slot * (D + 2);
+        float *dst = a.ws + slot * (D + kAttnHeader);
 #pragma unroll
-        for (int mt = 0; mt < MT; ++mt)
+        for (int mt = 0; mt < MT; ++mt) {
+            float o[4];
 #pragma unroll
             for (int i = 0; i < 4; ++i) {
                 const uint32_t dim = 16 * mt + 4 * g4 + i;
-                float o = 0.f;
+                o[i] = 0.f;
                 for (int w = 0; w < 4; ++w)
-                    o += so[(w * D + dim) * 16 + r16] * cw[w];
-                dst[2 + dim] = o;
+                    o[i] += so[(w * D + dim) * 16 + r16] * cw[w];
             }
+            *reinterpret_cast<float4 *>(dst + kAttnHeader + 16 * mt + 4 * g4) = make_float4(o[0], o[1], o[2], o[3]);
+        }
         if (g4 == 0) {
             // the reduce kernel merges with natural exponentials: store m in that base
             dst[0] = mm == -INFINITY ? -INFINITY : mm / kLog2e;

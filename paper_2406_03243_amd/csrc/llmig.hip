@@ -993,7 +993,7 @@ static int attn_workspace_bytes(int64_t num_layers, int64_t n_items, int64_t q_h
 {
     int64_t v = 0;
     if (__builtin_mul_overflow(num_layers, n_items, &v) || __builtin_mul_overflow(v, q_heads, &v) ||
-        __builtin_mul_overflow(v, (head_dim + 2) * 4, &v))
+        __builtin_mul_overflow(v, (head_dim + kAttnHeader) * 4, &v))
         return LLMIG_EINVAL;
     *bytes = v;
     return LLMIG_OK;
@@ -1013,7 +1013,7 @@ static int attn_check(const llmig_pool *pool, int32_t dtype, const void *q, int3
     if (q_heads % hkv != 0)
         return LLMIG_EINVAL;
     *fn = attn_kernel_for(dtype, pool->head_dim, q_heads / hkv);
-    if (!*fn || (reinterpret_cast<uintptr_t>(q) & 15u) || (reinterpret_cast<uintptr_t>(out) & 3u) ||
+    if (!*fn || (reinterpret_cast<uintptr_t>(q) & 15u) || (reinterpret_cast<uintptr_t>(out) & 15u) ||
         (reinterpret_cast<uintptr_t>(tables) & 3u))
         return LLMIG_EINVAL;
     for (int32_t b = 0; b < batch; ++b)
@@ -1086,7 +1086,8 @@ static int attn_enqueue(const llmig_pool *pool, const void *fn, const void *q, i
         r.seq_count[b] = (ctx_lens[b] + kPartTokens - 1) / kPartTokens;
         i += r.seq_count[b];
     }
-    const uint64_t total = static_cast<uint64_t>(pool->num_layers) * batch * q_heads * pool->head_dim;
+    // one lane per four dimensions of an output row
+    const uint64_t total = static_cast<uint64_t>(pool->num_layers) * batch * q_heads * (pool->head_dim / 4);
     const uint32_t grid = static_cast<uint32_t>(std::min<uint64_t>((total + kThreads - 1) / kThreads, 1u << 20));
     void *rargs[] = {&r};
     e = hipLaunchKernel(reinterpret_cast<const void *>(&attn_reduce), dim3(grid), dim3(kThreads), rargs, 0, st);
@@ -1116,7 +1117,7 @@ int llmig_decode_attention(const llmig_pool *pool, int32_t dtype, const void *q,
     int rc = attn_check(pool, dtype, q, batch, q_heads, tables, table_stride, ctx_lens, out, &fn, &n_items, &need);
     if (rc != LLMIG_OK)
         return rc;
-    if ((reinterpret_cast<uintptr_t>(workspace) & 3u) || (n_items > 0 && (!workspace || workspace_bytes < need)))
+    if ((reinterpret_cast<uintptr_t>(workspace) & 15u) || (n_items > 0 && (!workspace || workspace_bytes < need)))
         return LLMIG_EINVAL;
     return attn_enqueue(pool, fn, q, batch, q_heads, tables, table_stride, ctx_lens, scale,
                         static_cast<float *>(workspace), n_items, out, static_cast<hipStream_t>(stream));

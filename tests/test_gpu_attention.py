@@ -103,6 +103,11 @@ def test_decode_attention_rejects_unsupported():
         llmig_decode_attention(pool, q, tab, [40], 1.0, ws, out)
     with pytest.raises(LlmigError):                      # workspace too small
         llmig_decode_attention(pool, q, tab, [10], 1.0, ws[:16], out)
+    with pytest.raises(LlmigError):                      # workspace not 16-byte aligned
+        llmig_decode_attention(pool, q, tab, [10], 1.0, ws[4:], out)
+    out_off = torch.zeros(out.numel() + 1, dtype=torch.float32, device="cuda")[1:].view(out.shape)
+    with pytest.raises(LlmigError):                      # out not 16-byte aligned
+        llmig_decode_attention(pool, q, tab, [10], 1.0, ws, out_off)
     bad_q = [torch.zeros((2, 1, 4, 64), dtype=torch.float16, device="cuda"),   # layers
              torch.zeros((1, 1, 4, 128), dtype=torch.float16, device="cuda"),  # head_dim
              torch.zeros((1, 1, 4, 64), dtype=torch.bfloat16, device="cuda")]  # type
