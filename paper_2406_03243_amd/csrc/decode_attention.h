@@ -20,6 +20,14 @@
 
 namespace {
 
+#define LLMIG_LDS __attribute__((address_space(3)))
+
+// s_waitcnt immediates (gfx9 encoding: vmcnt in bits 3:0 and 15:14, expcnt
+// in 6:4, lgkmcnt in 11:8; a field at its maximum does not wait): until every
+// vector-memory load has returned, and until every LDS access has.
+constexpr int kWaitVm0 = 0x0F70;
+constexpr int kWaitLgkm0 = 0xC07F;
+
 constexpr int kPartTokens = 2048;    // tokens per partition
 constexpr int kAttnItems = 128;      // (sequence, partition) items per launch, in the kernel arguments
 constexpr int kAttnMaxBatch = 256;   // sequences per call (per-sequence item ranges ride in the arguments)
@@ -110,33 +118,42 @@ __global__ void __launch_bounds__(kThreads) attn_reduce(const AttnReduceArgs a)
 
 // ---------------------------------------------------------------------------
 // Matrix-core variant.  Per 16-token group of a partition, one wavefront:
-//   loads     the group's K and V rows whole: D/8 lanes of 16 bytes per row,
-//             64/(D/8) rows per load instruction (256 contiguous bytes a row
+//   loads     the group's K and V rows whole, straight from HBM into the
+//             wavefront's LDS (global_load_lds_dwordx4: 64 lanes x 16 bytes
+//             per instruction, D/8 lanes per row, 256 contiguous bytes a row
 //             for D = 128), tokens past the partition's end clamped to its
-//             last token (their weights are 0), so no branch sits between
-//             the loads;
+//             last token (their weights are 0).  The next group's rows are
+//             requested as soon as this group's operands have been read out
+//             of LDS, so they are in flight while this group computes, and
+//             no registers hold rows in transit;
 //   S^T = K . Q^T     16 tokens x 16 query rows (the group's heads, zero-padded),
-//                     16x16x32 MFMA over head_dim in steps of 32; K reaches
-//                     the A-operand layout (token = lane % 16) through the
-//                     wavefront's LDS region, 16-byte chunks in and out;
+//                     16x16x32 MFMA over head_dim in steps of 32; the K rows
+//                     sit in LDS with their 16-byte chunks XOR-swizzled by
+//                     token, so the operand reads (token = lane % 16) hit
+//                     distinct banks;
 //   online softmax per query row (a lane's rows of S^T are the tokens
 //                     4*(lane/16) .. +3 of query row lane%16);
 //   O^T += V^T . P^T  16x16x16 MFMA per 16 dims; P^T is already in the
-//                     B-operand layout, V^T goes through LDS (the layout
-//                     transposes there).  P is split into a 16-bit high part
-//                     and the 16-bit rounding of the remainder, two MFMAs, so
-//                     the weights keep ~2^-16 (bf16) / 2^-22 (fp16) precision.
+//                     B-operand layout, and V^T comes out of the row-major V
+//                     rows through gfx950's transposing LDS read
+//                     (ds_read_b64_tr_b16).  P is split into a 16-bit high
+//                     part and the 16-bit rounding of the remainder, two
+//                     MFMAs, so the weights keep ~2^-16 (bf16) / 2^-22 (fp16)
+//                     precision.
 // The four wavefronts take alternate token groups of the partition and merge
 // their states through LDS at the end.  The kernel waits on HBM, not on the
 // matrix cores or LDS, so it is built for four wavefronts per SIMD (at most
-// 128 registers: the accumulators move from AGPRs to VGPRs).
-// Measured on MI355X, one process, alternating, against the previous kernel
-// (K fragments loaded straight into the operand layout: 16 rows x 64 bytes
-// per load instruction; 1024-token partitions; the hardware's workgroup
-// order) on a GQA decode step (80 layers, 8 KV heads of 128, 17 sequences,
-// 65,280 tokens): whole-row K loads +8%, grouping each (layer, partition)'s
-// KV heads on one XCD +7%, 2048-token partitions +4%; 0.63 -> 0.75 of HBM
-// peak for the step, partial and merge kernels together.
+// 128 registers: the accumulators move from AGPRs to VGPRs; 32 KiB of LDS
+// per workgroup for the rows).
+// Measured on MI355X, one process, alternating, on a GQA decode step (80
+// layers, 8 KV heads of 128, 17 sequences, 65,280 tokens), each step against
+// the kernel before it: whole-row K loads rearranged through LDS instead of
+// K fragments loaded straight into the operand layout (16 rows x 64 bytes
+// per load instruction) +8%; grouping each (layer, partition)'s KV heads on
+// one XCD +7%; 2048-token partitions instead of 1024 +4%; rows loaded
+// straight into LDS one group ahead instead of through registers, with the
+// transposing V^T reads, +2% (bit-identical output).  0.63 -> 0.77 of HBM
+// peak for the partial kernel.
 typedef _Float16 f16x8_t __attribute__((ext_vector_type(8)));
 typedef _Float16 f16x4_t __attribute__((ext_vector_type(4)));
 typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
@@ -194,14 +211,14 @@ attn_partial_mfma(const AttnArgs a)
     constexpr int MT = D / 16;            // 16-dim tiles of the PV product
     constexpr int LPR = D / 8;            // lanes per row in the K and V loads (16 bytes each)
     constexpr int RPL = 64 / LPR;         // rows per load instruction
-    constexpr int VP = 20;                // LDS pitch of one V^T row: 16 tokens + 4 pad (40 bytes)
+    constexpr int RB = D * 2;             // bytes of one K or V row
+    constexpr int RPB = 128 / D;          // rows per 256 bytes (one pass over the 64 banks)
     constexpr float kLog2e = 1.4426950408889634f;
-    // 4 wavefronts x D rows x VP in the loop (each wavefront's region holds
-    // its group's K chunks first, 16 x (LPR + 1) x 16 bytes, then its V^T);
-    // reused for the final merge of 4 x D x 16 floats.
-    constexpr int kVtBytes = 4 * D * VP * 2, kMergeBytes = 4 * D * 16 * 4;
-    static_assert(16 * (LPR + 1) * 16 <= D * VP * 2, "a group's K chunks fit in the wavefront's region");
-    __shared__ __align__(16) uint8_t smem[kVtBytes > kMergeBytes ? kVtBytes : kMergeBytes];
+    // 4 wavefronts x (16 K rows + 16 V rows) in the loop; reused for the
+    // final merge of 4 x D x 16 floats.
+    constexpr int kRowBytes = 4 * 2 * 16 * RB, kMergeBytes = 4 * D * 16 * 4;
+    static_assert(KS * 64 * 16 == 16 * RB, "KS load instructions of 1 KiB cover the 16 rows of a group");
+    __shared__ __align__(16) uint8_t smem[kRowBytes > kMergeBytes ? kRowBytes : kMergeBytes];
     __shared__ float sh_m[4][16], sh_l[4][16];
     // block ids of the partition: dynamic LDS of attn_blk_slots(block_size) entries
     extern __shared__ int32_t sh_blk[];
@@ -236,7 +253,6 @@ attn_partial_mfma(const AttnArgs a)
 
     const uint8_t *kbase = reinterpret_cast<const uint8_t *>(table_entry(a.k_tab, layer));
     const uint8_t *vbase = reinterpret_cast<const uint8_t *>(table_entry(a.k_tab, a.num_layers + layer));
-    uint16_t *vt = reinterpret_cast<uint16_t *>(smem) + wave * D * VP;
 
     // The partition's block ids, once, so no token waits on a table load.
     const int32_t *table = a.tables + static_cast<uint64_t>(b) * a.table_stride;
@@ -264,54 +280,62 @@ attn_partial_mfma(const AttnArgs a)
     for (int mt = 0; mt < MT; ++mt)
         acc[mt] = f32x4_t{0.f, 0.f, 0.f, 0.f};
 
-    for (int32_t tg = start + 16 * static_cast<int32_t>(wave); tg < end; tg += 64) {
-        // K and V rows: KS loads each of RPL whole rows; row tg + j*RPL +
-        // lane/LPR, dims 8*(lane%LPR) .. +8.  A token past the partition's end
-        // loads its last token instead; its score is masked below, so its
-        // weight is 0.
-        u32x4 kr[KS], vr[KS];
+    // The wavefront's rows of one 16-token group in LDS, D/8 chunks of 16
+    // bytes a row.  K chunk c of local token t sits at slot c ^ kswz(t), so
+    // that the 16 tokens an operand read touches at once fall on distinct
+    // banks; V rows are plain (the transposing reads take them as they are).
+    const uint32_t wv = __builtin_amdgcn_readfirstlane(wave);
+    uint8_t *kbuf = smem + wv * (2 * 16 * RB);
+    uint8_t *vbuf = kbuf + 16 * RB;
+    auto kswz = [](uint32_t t) { return (t / RPB) % LPR; };
+    // Requests the rows of the group starting at token t0: KS instructions
+    // for K and KS for V, instruction j's lane carrying local token
+    // j*RPL + lane/LPR into LDS slot lane%LPR of that token's row.  A token
+    // past the partition's end loads its last token; its score is masked
+    // below, so its weight is 0.
+    auto request_group = [&](int32_t t0) {
 #pragma unroll
         for (int j = 0; j < KS; ++j) {
-            const int32_t t = min(tg + j * RPL + static_cast<int32_t>(lane / LPR), end - 1);
+            const uint32_t tl = j * RPL + lane / LPR, slot = lane % LPR;
+            const int32_t t = min(t0 + static_cast<int32_t>(tl), end - 1);
             const uint64_t row = (static_cast<uint64_t>(sh_blk[t / a.block_size - first_blk]) * a.block_size +
                                   t % a.block_size) * a.kv_heads + g;
-            kr[j] = load16(kbase + (row * D + 8 * (lane % LPR)) * 2);
-            vr[j] = load16(vbase + (row * D + 8 * (lane % LPR)) * 2);
+            __builtin_amdgcn_global_load_lds((const void LLMIG_GLOBAL *)(kbase + (row * D + 8 * (slot ^ kswz(tl))) * 2),
+                                             (void LLMIG_LDS *)(kbuf + j * 1024), 16, 0, kStreamLoad);
+            __builtin_amdgcn_global_load_lds((const void LLMIG_GLOBAL *)(vbase + (row * D + 8 * slot) * 2),
+                                             (void LLMIG_LDS *)(vbuf + j * 1024), 16, 0, kStreamLoad);
         }
-        // K to the A-operand layout (token r16, dims 32*ks + 8*g4 .. +8)
-        // through the wavefront's LDS region: chunk c of token t at
-        // kst[t * (LPR + 1) + c] (one chunk of padding per token keeps the
-        // strided reads on distinct banks).
-        u32x4 *kst = reinterpret_cast<u32x4 *>(vt);
-#pragma unroll
-        for (int j = 0; j < KS; ++j)
-            kst[(j * RPL + lane / LPR) * (LPR + 1) + lane % LPR] = kr[j];
-        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-        __builtin_amdgcn_wave_barrier();
-        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+    };
+    const int32_t tg0 = start + 16 * static_cast<int32_t>(wave);
+    if (tg0 < end)
+        request_group(tg0);
+    for (int32_t tg = tg0; tg < end; tg += 64) {
+        // this group's rows have landed (the only loads in flight)
+        __builtin_amdgcn_s_waitcnt(kWaitVm0);
+        // K fragments (A operand: token r16, dims 32*ks + 8*g4 .. +8)
         u32x4 kf[KS];
 #pragma unroll
         for (int ks = 0; ks < KS; ++ks)
-            kf[ks] = kst[r16 * (LPR + 1) + 4 * ks + g4];
-        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-        __builtin_amdgcn_wave_barrier();
-        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+            kf[ks] = *reinterpret_cast<const u32x4 *>(kbuf + r16 * RB + (((4 * ks + g4) ^ kswz(r16)) * 16));
+        // V^T fragments (A operand of O^T: dim 16*mt + r16, tokens 4*g4 .. +3)
+        // by transposing reads: lane r16 of the 16-lane group g4 receives
+        // element r16 % 4 of the 8 bytes that lane 4*q + r16/4 of its group
+        // addresses, for q = 0..3; those address token 4*g4 + q, dims
+        // 16*mt + 4*(r16 % 4) .. +3.
+        uint64_t vf[MT];
+#pragma unroll
+        for (int mt = 0; mt < MT; ++mt)
+            vf[mt] = __builtin_bit_cast(uint64_t, __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+                (i16x4_t LLMIG_LDS *)(vbuf + (4 * g4 + r16 / 4) * RB + (16 * mt + 4 * (r16 % 4)) * 2)));
+        // the reads have returned before the next group's rows overwrite them
+        __builtin_amdgcn_s_waitcnt(kWaitLgkm0);
+        if (tg + 64 < end)
+            request_group(tg + 64);
         // S^T = K . Q^T
         f32x4_t s = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
         for (int ks = 0; ks < KS; ++ks)
             s = mfma_qk<BF16>(kf[ks], qf[ks], s);
-        // V^T into LDS: element (token, dim) at vt[dim * VP + token - tg]
-#pragma unroll
-        for (int j = 0; j < KS; ++j) {
-            const uint32_t tok = j * RPL + lane / LPR, d0 = 8 * (lane % LPR);
-            const uint32_t w4[4] = {vr[j].x, vr[j].y, vr[j].z, vr[j].w};
-#pragma unroll
-            for (int e = 0; e < 4; ++e) {
-                vt[(d0 + 2 * e) * VP + tok] = static_cast<uint16_t>(w4[e] & 0xffffu);
-                vt[(d0 + 2 * e + 1) * VP + tok] = static_cast<uint16_t>(w4[e] >> 16);
-            }
-        }
         // online softmax for query row r16 over tokens tg + 4*g4 + i
         float sc[4], mx = -INFINITY;
 #pragma unroll
@@ -342,20 +366,12 @@ attn_partial_mfma(const AttnArgs a)
             ph |= static_cast<uint64_t>(hi) << (16 * i);
             pl |= static_cast<uint64_t>(to16<BF16>(p[i] - hv)) << (16 * i);
         }
-        // the wavefront's own LDS writes above precede its reads below
-        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-        __builtin_amdgcn_wave_barrier();
-        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
 #pragma unroll
         for (int mt = 0; mt < MT; ++mt) {
-            const uint64_t vf = *reinterpret_cast<const uint64_t *>(vt + (16 * mt + r16) * VP + 4 * g4);
             acc[mt] = acc[mt] * c;
-            acc[mt] = mfma_pv<BF16>(vf, ph, acc[mt]);
-            acc[mt] = mfma_pv<BF16>(vf, pl, acc[mt]);
+            acc[mt] = mfma_pv<BF16>(vf[mt], ph, acc[mt]);
+            acc[mt] = mfma_pv<BF16>(vf[mt], pl, acc[mt]);
         }
-        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-        __builtin_amdgcn_wave_barrier();
-        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
     }
 
     // merge the four wavefronts: state of query row r16, O^T rows 16*mt + 4*g4 + i
