@@ -211,7 +211,11 @@ int scratch_pointer(int device, void **out)
 // 64-bit tickets, one cache line apart, in pinned host memory mapped for
 // every device, allocated with the first pool (set-up) and kept for the
 // process.  Each call takes the next ticket from a counter; its slot is
-// ticket % kFinishSlots, and a slot only ever receives larger tickets.
+// ticket % kFinishSlots, and it returns only on reading its own ticket
+// there.  A slot can be rewritten by a call kFinishSlots tickets later (on
+// another stream, in either order); a waiter whose ticket was overwritten
+// before it read it falls back to the runtime wait, so no call returns
+// before its own work is done.
 constexpr uint64_t kFinishSlots = 1024;
 constexpr uint64_t kFinishSlotStride = 64 / sizeof(uint64_t);
 // How long llmig_migration_finish reads its slot before it falls back to a
@@ -271,7 +275,7 @@ int wait_stream(int device, hipStream_t stream)
         const uint64_t *hp = g_finish.host.load() + slot;
         const auto t0 = std::chrono::steady_clock::now();
         for (uint32_t k = 1;; ++k) {
-            if (__atomic_load_n(hp, __ATOMIC_ACQUIRE) >= ticket)
+            if (__atomic_load_n(hp, __ATOMIC_ACQUIRE) == ticket)
                 return LLMIG_OK;
             if ((k & 1023u) == 0 &&
                 std::chrono::duration<double, std::micro>(std::chrono::steady_clock::now() - t0).count() >
