@@ -656,7 +656,7 @@ def xlayout_section(reps=20):
     return out
 
 
-def load_section(reps=3, reader_passes=3, step_ms=20.0, caps=(0, 256, 64)):
+def load_section(reps=5, reader_passes=3, step_ms=20.0, caps=(0, 256, 64)):
     """GQA long-context migration beside a streaming reader of a separate
     40 GB region (all streams at the default priority), for several caps on
     the migration's copy grid (0: uncapped)."""
