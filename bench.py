@@ -233,7 +233,8 @@ def main():
         b = stage_bytes(rec.blocks, shape, src.tile_bytes)
         entry = {"tokens": [rec.from_tok, rec.to_tok], "blocks": rec.blocks, "bytes": b, "final": rec.final,
                  "gpu_us_median": round(statistics.median(us), 2), "gpu_us": spread(us),
-                 "GBps": round(b / (statistics.median(us) * 1e-6) / 1e9, 1), "timed_in": timed_in}
+                 "GBps": round(b / (statistics.median(us) * 1e-6) / 1e9, 1),
+                 "hbm_frac": round(b / (statistics.median(us) * 1e-6) / 1e9 / HBM_PEAK_GBS, 3), "timed_in": timed_in}
         stages.append(entry)
 
     result = {
@@ -447,6 +448,7 @@ def downtime_sweep(reps):
             "stage1_blocks": s1[0].blocks,
             "stage1_us": round(s1_us, 1),
             "stage1_GBps": round(s1_bytes / (s1_us * 1e-6) / 1e9, 1),
+            "stage1_hbm_frac": round(s1_bytes / (s1_us * 1e-6) / 1e9 / HBM_PEAK_GBS, 3),
             "final_blocks": res[0][0].stages[-1].blocks,
             "downtime_us_median": round(statistics.median(dt for _, dt in res), 1),
             "downtime_us_min": round(min(dt for _, dt in res), 1),
@@ -493,6 +495,7 @@ def batched_section(reps=20, host_reps=3, chunk_pairs=64, cpu=True):
            "pool_blocks": shape.num_blocks, "bytes": nbytes, "stage_us_median": round(us, 1),
            "stage_us": spread(times),
            "GBps": round(nbytes / (us * 1e-6) / 1e9, 1),
+           "hbm_frac": round(nbytes / (us * 1e-6) / 1e9 / HBM_PEAK_GBS, 3),
            "lengths": {"min": int(min(su.lengths)), "median": float(statistics.median(su.lengths)),
                        "max": int(max(su.lengths)), "tokens": int(sum(su.lengths))}}
     # block fusion with device staging: the pack and unpack kernels alone,
@@ -722,6 +725,7 @@ def load_section(reps=5, reader_passes=3, step_ms=20.0, caps=(0, 256, 64)):
             "reader_slowdown_during_migration": round(max(0.0, r_both - r_alone) / t_mig, 3),
             "migration_wall_us": round(t_mig, 1),
             "stage1_GBps_alone": round(s1_bytes / (s1_alone * 1e-6) / 1e9, 1),
+            "stage1_hbm_frac_alone": round(s1_bytes / (s1_alone * 1e-6) / 1e9 / HBM_PEAK_GBS, 3),
             "stage1_GBps_under_load": round(s1_bytes / (s1_both * 1e-6) / 1e9, 1),
             "stages_under_load": statistics.median(len(b[1].stages) for b in both),
             "downtime_us_alone": round(statistics.median(dt for _, dt in alone_m), 1),
