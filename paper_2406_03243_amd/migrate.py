@@ -200,6 +200,8 @@ def run_scheduled(src: Pool, dst: Pool, src_table, dst_free_list, initial_len: i
     """A migration whose decoding appends a known batch of tokens before each
     incremental stage (``appends`` is a list of device tensors laid out
     [L][K,V][n_tok][slot_bytes]); the stage after the last batch is final.
+    Each stage is planned after the host has seen the batch before it
+    written.
     Stage 0 is timed with events on the migration stream; the incremental
     stages too when ``time_all``, the final one when ``time_final`` (its
     events then add their own host work to the downtime).  Returns
@@ -226,7 +228,12 @@ def run_scheduled(src: Pool, dst: Pool, src_table, dst_free_list, initial_len: i
             m.finish(length, time_it=time_final)
             downtime_us = (m.finished_at - t0) * 1e6
         else:
-            mig_stream.wait_event(ev)
+            # The next stage is planned once the host has seen this batch
+            # written, as an engine plans it after the decode step that
+            # produced its tokens; the batch is then complete and the stage
+            # needs no wait on the decode stream.  (The host waits while
+            # stage 0 still copies, so the wait costs the GPU nothing.)
+            ev.synchronize()
             m.stage(length, final=False, time_it=time_all)
     if downtime_us is None:
         t0 = time.perf_counter()
