@@ -128,6 +128,18 @@ def _stream(stream) -> int:
     return stream.cuda_stream
 
 
+def _used_on(stream, *tensors) -> None:
+    """Tells torch's caching allocator that the device tensors are read or
+    written by work on ``stream`` (a torch stream): a tensor the caller drops
+    right after the call is then not handed out again before that work has
+    run.  Raw stream handles carry no such record; their callers keep the
+    tensors alive themselves."""
+    if isinstance(stream, torch.cuda.Stream):
+        for t in tensors:
+            if isinstance(t, torch.Tensor) and t.is_cuda:
+                t.record_stream(stream)
+
+
 def _host_i32(a) -> np.ndarray:
     return np.ascontiguousarray(np.asarray(a, dtype=np.int32))
 
@@ -228,6 +240,7 @@ def llmig_stage(src: Pool, dst: Pool, map_src, map_dst, stream=None) -> None:
     if ns != nd or ds != dd:
         raise ValueError("map_src and map_dst must have one length and one location")
     _check(_lib.llmig_stage(src.handle, dst.handle, ps, pd, ns, ds, _stream(stream)), "llmig_stage")
+    _used_on(stream, map_src, map_dst)
 
 
 def _staging(staging: torch.Tensor):
@@ -243,6 +256,7 @@ def llmig_pack(src: Pool, blocks, staging: torch.Tensor, stream=None) -> None:
     pb, n, on_dev, keep = _ids(blocks)
     ptr, nbytes = _staging(staging)
     _check(_lib.llmig_pack(src.handle, pb, n, on_dev, ptr, nbytes, _stream(stream)), "llmig_pack")
+    _used_on(stream, blocks, staging)
 
 
 def llmig_unpack(dst: Pool, blocks, staging: torch.Tensor, stream=None) -> None:
@@ -250,6 +264,7 @@ def llmig_unpack(dst: Pool, blocks, staging: torch.Tensor, stream=None) -> None:
     pb, n, on_dev, keep = _ids(blocks)
     ptr, nbytes = _staging(staging)
     _check(_lib.llmig_unpack(dst.handle, pb, n, on_dev, ptr, nbytes, _stream(stream)), "llmig_unpack")
+    _used_on(stream, blocks, staging)
 
 
 def llmig_unpack_layout(dst: Pool, blocks, staging: torch.Tensor, staging_layouts, stream=None) -> None:
@@ -259,6 +274,7 @@ def llmig_unpack_layout(dst: Pool, blocks, staging: torch.Tensor, staging_layout
     ptr, nbytes = _staging(staging)
     _check(_lib.llmig_unpack_layout(dst.handle, pb, n, on_dev, ptr, nbytes, int(staging_layouts[0]),
                                     int(staging_layouts[1]), _stream(stream)), "llmig_unpack_layout")
+    _used_on(stream, blocks, staging)
 
 
 def llmig_write_tokens(pool: Pool, table, from_tok: int, data: torch.Tensor, stream=None) -> None:
@@ -273,6 +289,7 @@ def llmig_write_tokens(pool: Pool, table, from_tok: int, data: torch.Tensor, str
     t = _host_i32(table)
     _check(_lib.llmig_write_tokens(pool.handle, t.ctypes.data, t.size, int(from_tok), nbytes // per_tok,
                                    data.data_ptr(), _stream(stream)), "llmig_write_tokens")
+    _used_on(stream, data)
 
 
 MIGRATION_STATES = {0: "ACTIVE", 1: "FINISHED", 2: "COMMITTED", 3: "ABORTED"}
@@ -433,6 +450,7 @@ def llmig_decode_attention(pool: Pool, q: torch.Tensor, tables: torch.Tensor, ct
                                        c.ctypes.data, float(scale), workspace.data_ptr(),
                                        workspace.numel() * workspace.element_size(), out.data_ptr(),
                                        _stream(stream)), "llmig_decode_attention")
+    _used_on(stream, q, tables, workspace, out)
 
 
 def llmig_stream_read(region: torch.Tensor, passes: int, workgroups: int, out: torch.Tensor, stream=None) -> None:
@@ -444,6 +462,7 @@ def llmig_stream_read(region: torch.Tensor, passes: int, workgroups: int, out: t
     _check(_lib.llmig_stream_read(region.data_ptr(), region.numel() * region.element_size(), int(passes),
                                   int(workgroups), out.data_ptr(), out.numel(), _stream(stream)),
            "llmig_stream_read")
+    _used_on(stream, region, out)
 
 
 def llmig_decode_attention_noalloc(pool: Pool, q: torch.Tensor, tables: torch.Tensor, ctx_lens, scale: float,
@@ -456,3 +475,4 @@ def llmig_decode_attention_noalloc(pool: Pool, q: torch.Tensor, tables: torch.Te
                                                q.shape[1], q.shape[2], tables.data_ptr(), tables.shape[1],
                                                c.ctypes.data, float(scale), out.data_ptr(), _stream(stream)),
            "llmig_decode_attention_noalloc")
+    _used_on(stream, q, tables, out)

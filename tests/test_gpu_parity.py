@@ -208,6 +208,56 @@ def test_multistage_scheduled_small():
     assert downtime > 0
 
 
+@pytest.mark.parametrize("driver", ["scheduled", "timed"])
+def test_migration_waits_for_decode_writes_in_flight(driver):
+    """A migration that starts while the decode stream still has work queued
+    (a long read, then the write of the request's last 20 tokens): its first
+    stage must copy those tokens as written, so it waits for the decode
+    stream (the drivers skip that wait only when the stream is idle).  The
+    write's data is a temporary the caller drops at once and the test then
+    allocates more device memory: the binding must keep the dropped tensor's
+    memory from being handed out again while the write is still queued."""
+    shape = wl.PoolShape(4, 300, 16, 4, 64, "fp16")
+    seed, initial = 7373, 1000
+    say("migration behind queued decode writes", driver, shape, initial)
+    src = make_pool(shape, seed, wl.SRC_VALUES)
+    dst = make_pool(shape, seed, wl.DST_VALUES)
+    table, _ = wl.request_table(seed, shape.num_blocks, 80, 0.3)
+    free, _ = wl.free_list(seed, shape.num_blocks, 0.3)
+    (late,) = _appends(shape, seed + 1, [20], src.slot_bytes)
+    hs, hd = host_image(src), host_image(dst)
+    oracle.default().write_tokens(hs, table, initial - 20, late)    # what the queued write leaves
+    mig, dec = harness.concurrent_streams(2)[0]
+    region = torch.zeros(1 << 30, dtype=torch.uint8, device="cuda")
+    sink = torch.empty(1024 * 256, dtype=torch.int64, device="cuda")
+    torch.cuda.synchronize()
+    llmig.llmig_stream_read(region, 4, 1024, sink, stream=dec)        # ~1 ms of queued decode work
+    llmig.llmig_write_tokens(src, table, initial - 20, torch.from_numpy(late).cuda(), stream=dec)
+    assert not dec.query()
+    (append_pool,) = _appends(shape, seed + 2, [64], src.slot_bytes)
+    if driver == "scheduled":
+        m, _ = migrate.run_scheduled(src, dst, table, free, initial, [], mig, dec)
+    else:
+        m, _ = migrate.run_timed(src, dst, table, initial, free, torch.from_numpy(append_pool).cuda(), mig, dec,
+                                 step_ms=20.0)
+    torch.cuda.synchronize()
+    # replay the recorded schedule: tokens appended by the timed driver come
+    # from the head of its append pool
+    events, cur = [], initial
+    for r in m.stages:
+        if r.length > cur:
+            events.append(("append", cur, np.ascontiguousarray(append_pool[:, :, cur - initial:r.length - initial])))
+            cur = r.length
+        events.append(("stage", r.length, r.from_tok, r.to_tok))
+    final_len = cur
+    assert m.stages[-1].final and m.stages[0].from_tok == 0
+    dst_table, _ = oracle.default().migrate(hs, hd, table, free, events)
+    gs, gd = host_image(src), host_image(dst)
+    assert_same(gs, hs, "source (with the queued write)")
+    assert_same(gd, hd, "destination")
+    assert oracle.default().first_token_mismatch(gs, table, gd, dst_table, final_len) == -1
+
+
 def test_multistage_timed_small():
     shape = wl.PoolShape(6, 600, 16, 13, 128, "fp16")
     seed, initial = 6262, 4096
