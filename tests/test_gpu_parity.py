@@ -420,6 +420,43 @@ def test_coordinator_finish_waits_and_refuses():
     assert oracle.default().first_token_mismatch(hs, table, host_image(dst), got, 355) == -1
 
 
+def test_finish_behind_long_work_on_its_stream():
+    """llmig_migration_finish queued behind more work on its stream than its
+    completion slot is read for (32 GiB of streaming reads, at least 4.3 ms
+    at the HBM peak, against a 2 ms spin), so its wait ends through the
+    runtime: it returns only once everything before it on the stream is
+    done.  The reader's per-lane sums and the final stage's blocks are read
+    back right away, with no synchronisation of the stream, and are whole."""
+    import time
+    shape = wl.PoolShape(2, 150, 16, 4, 64, "fp16")
+    say("finish behind long work", shape)
+    src = make_pool(shape, 93, wl.SRC_VALUES)
+    dst = make_pool(shape, 93, wl.DST_VALUES)
+    table, _ = wl.request_table(93, shape.num_blocks, 40)
+    free, _ = wl.free_list(93, shape.num_blocks)
+    hs, hd = host_image(src), host_image(dst)
+    mig = torch.cuda.Stream()
+    m = migrate.Migration(src, dst, table, free, mig)
+    m.stage(320, final=False)
+    region_bytes, passes, workgroups = 2 << 30, 16, 1024
+    region = torch.ones(region_bytes // 4, dtype=torch.int32, device="cuda")
+    out = torch.zeros(workgroups * 256, dtype=torch.int64, device="cuda")
+    torch.cuda.synchronize()
+    llmig.llmig_stream_read(region, passes, workgroups, out, stream=mig)
+    t0 = time.perf_counter()
+    rec = m.finish(355)
+    waited = time.perf_counter() - t0
+    sums = out.cpu().numpy()                 # on the default stream: not ordered after the migration's
+    got = m.commit()
+    assert rec.final and rec.blocks == 3
+    assert waited >= passes * region_bytes / 8e12, waited
+    # every lane read passes * words / lanes words of four ones: each 32-bit half of its folded sum is twice that
+    c = 2 * passes * (region_bytes // 16) // (workgroups * 256)
+    assert np.all(sums == (c << 32) | c), np.unique(sums)[:5]
+    oracle.default().copy(hs, hd, table[:23], got)
+    assert_same(host_image(dst), hd, "destination after finish")
+
+
 @pytest.mark.parametrize("cap", [1, 7, 64])
 def test_capped_grid_multistage(cap):
     """Throttled migrations: a capped grid walks many items per workgroup."""
