@@ -109,8 +109,9 @@ typedef struct llmig_pool llmig_pool;
  * device's copy of the scratch array of llmig_decode_attention_noalloc and
  * maps the completion slots of llmig_migration_finish (a few KB of pinned
  * host memory, allocated once per process and kept until it ends); should
- * either fail, the calls that use them fall back or report it themselves.  Errors: LLMIG_EINVAL (a non-positive size, a null array or
- * address, misalignment, a tile over 2^31 bytes), LLMIG_EHIP.
+ * either fail, the calls that use them fall back or report it themselves.
+ * Errors: LLMIG_EINVAL (a non-positive size, a null array or address,
+ * misalignment, a tile over 2^31 bytes), LLMIG_EHIP.
  *
  * Every call that enqueues work on a pool (stage, pack, unpack, write_tokens,
  * decode attention, the coordinator's stage) must be made with the pool's
