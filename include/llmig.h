@@ -381,6 +381,32 @@ int llmig_decode_attention(const llmig_pool *pool, int32_t dtype, const void *q,
                            const int32_t *ctx_lens, float scale, void *workspace,
                            int64_t workspace_bytes, float *out, void *stream);
 
+/* A migration stage carried by a decode step (§4.2's stage copy of a request
+ * that is still decoding, §6.2's cost of it to the batch): exactly
+ * llmig_decode_attention on `pool`, which in the same pass also writes the
+ * whole blocks [from_block, to_block) of sequence `seq` into `dst`: logical
+ * block j (source block tables[seq * table_stride + j]) lands in dst block
+ * dst_ids[j - from_block], every layer, K and V, byte for byte as
+ * llmig_stage would copy the same pairs.  The attention reads those bytes
+ * from HBM anyway; the stage adds only their writes, so it costs the decode
+ * batch about half of what a separate stage copy beside it would.
+ * dst: a second pool on the same device, of the same geometry and (NHD)
+ * layouts, not overlapping `pool`.  dst_ids: DEVICE int32 array of
+ * to_block - from_block ids, 4-byte aligned, valid until the work
+ * completes; the caller guarantees they are in [0, dst's num_blocks) and
+ * distinct (as for llmig_stage with map_on_device = 1), which the
+ * coordinator's llmig_migration_next gives.  Only whole blocks:
+ * to_block * block_size <= ctx_lens[seq].  from_block == to_block is
+ * llmig_decode_attention.  Errors: those of llmig_decode_attention, and
+ * LLMIG_EINVAL for a bad seq, block range, dst or dst_ids; nothing is
+ * enqueued on an error. */
+int llmig_decode_attention_migrate(const llmig_pool *pool, int32_t dtype, const void *q, int32_t batch,
+                                   int32_t q_heads, const int32_t *tables, int32_t table_stride,
+                                   const int32_t *ctx_lens, float scale, void *workspace,
+                                   int64_t workspace_bytes, float *out, const llmig_pool *dst,
+                                   int32_t seq, const int32_t *dst_ids, int64_t from_block,
+                                   int64_t to_block, void *stream);
+
 /* ---------------------------------------------------------------------------
  * For callers that cannot allocate device memory: code being captured into a
  * HIP graph, serving loops that must not call hipMalloc, harnesses that

@@ -49,6 +49,12 @@ struct AttnArgs {
     int32_t item_seq[kAttnItems];
     int32_t item_start[kAttnItems];
     int32_t item_end[kAttnItems];
+    // The stage copy a migrating launch carries (read only when it does):
+    // logical blocks [mig_from, mig_to) of sequence mig_seq go to the blocks
+    // mig_ids[j - mig_from] of the pool whose K and V bases dst_tab lists.
+    const uint64_t *dst_tab;
+    const int32_t *mig_ids;
+    int32_t mig_seq, mig_from, mig_to;
 };
 
 struct AttnReduceArgs {
@@ -197,13 +203,23 @@ __device__ __forceinline__ uint32_t to16(float x)
 // Block ids a partition can touch, for the dynamic LDS of attn_partial_mfma:
 // a partition starts on a block boundary (kPartTokens is a multiple of every
 // block size that divides it) or inside a block, so at most
-// ceil(kPartTokens / block_size) + 1 blocks.
-inline uint32_t attn_blk_slots(uint32_t block_size)
+// ceil(kPartTokens / block_size) + 1 blocks.  A migrating launch keeps the
+// destination id of each of them beside it.
+__host__ __device__ inline uint32_t attn_blk_slots(uint32_t block_size)
 {
     return (kPartTokens + block_size - 1) / block_size + 1;
 }
 
-template <int BF16, int D>
+// MIG: the launch also carries a migration stage of one sequence (Llumnix
+// §4.2 stage copy, done as a side effect of decode's reads).  Every
+// wavefront already brings its token group's K and V rows (one KV head's
+// D * 2 bytes of each token) into LDS; for the tokens of the stage's blocks
+// it reads them back out of LDS and stores them, unchanged, at the same
+// place in the destination blocks.  Across the kv_heads workgroups of every
+// (layer, partition) that covers each whole tile, K and V, of those blocks,
+// so the destination receives exactly the bytes a pool-to-pool stage copy
+// would write, while HBM reads them once, for the attention.
+template <int BF16, int D, int MIG>
 __global__ void __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(4, 8)))
 attn_partial_mfma(const AttnArgs a)
 {
@@ -220,7 +236,8 @@ attn_partial_mfma(const AttnArgs a)
     static_assert(KS * 64 * 16 == 16 * RB, "KS load instructions of 1 KiB cover the 16 rows of a group");
     __shared__ __align__(16) uint8_t smem[kRowBytes > kMergeBytes ? kRowBytes : kMergeBytes];
     __shared__ float sh_m[4][16], sh_l[4][16];
-    // block ids of the partition: dynamic LDS of attn_blk_slots(block_size) entries
+    // block ids of the partition: dynamic LDS of attn_blk_slots(block_size)
+    // entries (a migrating launch: twice that, the destination ids after them)
     extern __shared__ int32_t sh_blk[];
 
     // The dispatcher deals workgroups to the eight XCDs in turn.  Renumbered
@@ -260,6 +277,17 @@ attn_partial_mfma(const AttnArgs a)
     const int32_t n_blk = (end - 1) / static_cast<int32_t>(a.block_size) - first_blk + 1;
     for (int32_t k = threadIdx.x; k < n_blk; k += kThreads)
         sh_blk[k] = table[first_blk + k];
+    // A migrating launch: whether this workgroup's rows are the migrating
+    // sequence's, and the destination block of each of its logical blocks
+    // (-1 outside the stage).
+    const bool mig = MIG && static_cast<int32_t>(b) == a.mig_seq;
+    int32_t *sh_dst = sh_blk + attn_blk_slots(a.block_size);
+    if (mig) {
+        for (int32_t k = threadIdx.x; k < n_blk; k += kThreads) {
+            const int32_t j = first_blk + k;
+            sh_dst[k] = j >= a.mig_from && j < a.mig_to ? a.mig_ids[j - a.mig_from] : -1;
+        }
+    }
     __syncthreads();
 
     // Q^T fragments (B operand): query row r16 of the group, dims 32*ks + 8*g4 .. +8.
@@ -306,12 +334,55 @@ attn_partial_mfma(const AttnArgs a)
                                              (void LLMIG_LDS *)(vbuf + j * 1024), 16, 0, kStreamLoad);
         }
     };
+    // A migrating launch: stores the group's rows that belong to the stage's
+    // blocks into the destination pool.  Lane `lane` of load instruction j
+    // brought token j*RPL + lane/LPR's chunk lane%LPR of the row (K: the
+    // swizzled slot of the chunk) into LDS at j * 1024 + lane * 16; it reads
+    // that back and stores it where the chunk lives in the destination tile:
+    // (slot of the token, head g, the chunk).  Rows of tokens past the
+    // partition's end (loaded as copies of its last token) are skipped.
+    auto store_group = [&](int32_t tg) {
+        uint8_t *const dk = reinterpret_cast<uint8_t *>(table_entry(a.dst_tab, layer));
+        uint8_t *const dv = reinterpret_cast<uint8_t *>(table_entry(a.dst_tab, a.num_layers + layer));
+        const uint64_t tile = static_cast<uint64_t>(a.block_size) * a.kv_heads * RB;
+        int32_t dst_blk[KS];
+        u32x4 r[KS];
+#pragma unroll
+        for (int j = 0; j < KS; ++j) {
+            const int32_t t = tg + j * RPL + static_cast<int32_t>(lane / LPR);
+            dst_blk[j] = t < end ? sh_dst[t / static_cast<int32_t>(a.block_size) - first_blk] : -1;
+            r[j] = *reinterpret_cast<const u32x4 *>(kbuf + j * 1024 + lane * 16);
+        }
+        __builtin_amdgcn_s_waitcnt(kWaitLgkm0);
+        // where lane's row of instruction j starts in its destination tiles
+        auto row_off = [&](int j) {
+            const int32_t t = tg + j * RPL + static_cast<int32_t>(lane / LPR);
+            return static_cast<uint64_t>(dst_blk[j]) * tile +
+                   (static_cast<uint64_t>(t % static_cast<int32_t>(a.block_size)) * a.kv_heads + g) * RB;
+        };
+#pragma unroll
+        for (int j = 0; j < KS; ++j)
+            if (dst_blk[j] >= 0)
+                store16(dk + row_off(j) + 16 * ((lane % LPR) ^ kswz(j * RPL + lane / LPR)), r[j]);
+#pragma unroll
+        for (int j = 0; j < KS; ++j)
+            r[j] = *reinterpret_cast<const u32x4 *>(vbuf + j * 1024 + lane * 16);
+        __builtin_amdgcn_s_waitcnt(kWaitLgkm0);
+#pragma unroll
+        for (int j = 0; j < KS; ++j)
+            if (dst_blk[j] >= 0)
+                store16(dv + row_off(j) + 16 * (lane % LPR), r[j]);
+    };
     const int32_t tg0 = start + 16 * static_cast<int32_t>(wave);
     if (tg0 < end)
         request_group(tg0);
     for (int32_t tg = tg0; tg < end; tg += 64) {
         // this group's rows have landed (the only loads in flight)
         __builtin_amdgcn_s_waitcnt(kWaitVm0);
+        // a migrating launch stores the stage's rows first, while no operand
+        // fragments are live yet
+        if (MIG && mig)
+            store_group(tg);
         // K fragments (A operand: token r16, dims 32*ks + 8*g4 .. +8)
         u32x4 kf[KS];
 #pragma unroll
@@ -420,19 +491,20 @@ attn_partial_mfma(const AttnArgs a)
 }
 
 template <int BF16, int D>
-const void *attn_kernel(int group)
+const void *attn_kernel(int group, bool migrating)
 {
-    if (group >= 1 && group <= 16 && (group & (group - 1)) == 0)
-        return reinterpret_cast<const void *>(&attn_partial_mfma<BF16, D>);
-    return nullptr;
+    if (group < 1 || group > 16 || (group & (group - 1)) != 0)
+        return nullptr;
+    return migrating ? reinterpret_cast<const void *>(&attn_partial_mfma<BF16, D, 1>)
+                     : reinterpret_cast<const void *>(&attn_partial_mfma<BF16, D, 0>);
 }
 
-const void *attn_kernel_for(int bf16, int head_dim, int group)
+const void *attn_kernel_for(int bf16, int head_dim, int group, bool migrating)
 {
     if (head_dim == 64)
-        return bf16 ? attn_kernel<1, 64>(group) : attn_kernel<0, 64>(group);
+        return bf16 ? attn_kernel<1, 64>(group, migrating) : attn_kernel<0, 64>(group, migrating);
     if (head_dim == 128)
-        return bf16 ? attn_kernel<1, 128>(group) : attn_kernel<0, 128>(group);
+        return bf16 ? attn_kernel<1, 128>(group, migrating) : attn_kernel<0, 128>(group, migrating);
     return nullptr;
 }
 

@@ -1007,7 +1007,7 @@ static int attn_workspace_bytes(int64_t num_layers, int64_t n_items, int64_t q_h
 // on success gives the kernel, the item count and the workspace size.
 static int attn_check(const llmig_pool *pool, int32_t dtype, const void *q, int32_t batch, int32_t q_heads,
                       const int32_t *tables, int32_t table_stride, const int32_t *ctx_lens, const float *out,
-                      const void **fn, int64_t *n_items, int64_t *ws_bytes)
+                      const void **fn, int64_t *n_items, int64_t *ws_bytes, bool migrating = false)
 {
     if (!pool || !on_current_device(pool) || (dtype != 0 && dtype != 1) || pool->elem_bytes != 2 || !q ||
         !tables || !ctx_lens || !out || batch < 1 || batch > kAttnMaxBatch || q_heads < 1 || table_stride < 1 ||
@@ -1016,7 +1016,7 @@ static int attn_check(const llmig_pool *pool, int32_t dtype, const void *q, int3
     const int32_t hkv = pool->num_kv_heads;
     if (q_heads % hkv != 0)
         return LLMIG_EINVAL;
-    *fn = attn_kernel_for(dtype, pool->head_dim, q_heads / hkv);
+    *fn = attn_kernel_for(dtype, pool->head_dim, q_heads / hkv, migrating);
     if (!*fn || (reinterpret_cast<uintptr_t>(q) & 15u) || (reinterpret_cast<uintptr_t>(out) & 15u) ||
         (reinterpret_cast<uintptr_t>(tables) & 3u))
         return LLMIG_EINVAL;
@@ -1028,15 +1028,34 @@ static int attn_check(const llmig_pool *pool, int32_t dtype, const void *q, int3
     return attn_workspace_bytes(pool->num_layers, *n_items, q_heads, pool->head_dim, ws_bytes);
 }
 
+// A stage copy carried by a decode-attention launch: logical blocks
+// [from, to) of sequence seq into the blocks ids[j - from] of dst.
+struct AttnMigration {
+    const llmig_pool *dst = nullptr;
+    int32_t seq = -1;
+    const int32_t *ids = nullptr;
+    int32_t from = 0, to = 0;
+};
+
 // Enqueues a checked decode-attention call: the partial kernel over the
 // items, kAttnItems per launch (their ranges ride in the kernel arguments),
 // then the merge.  ws holds the partial results.  Allocates nothing.
 static int attn_enqueue(const llmig_pool *pool, const void *fn, const void *q, int32_t batch, int32_t q_heads,
                         const int32_t *tables, int32_t table_stride, const int32_t *ctx_lens, float scale,
-                        float *ws, int64_t n_items, float *out, hipStream_t st)
+                        float *ws, int64_t n_items, float *out, hipStream_t st,
+                        const AttnMigration &mig = AttnMigration())
 {
     AttnArgs a;
     std::memset(&a, 0, sizeof(a));
+    a.mig_seq = -1;
+    if (mig.dst) {
+        a.dst_tab = mig.dst->d_tab;
+        a.mig_ids = mig.ids;
+        a.mig_seq = mig.seq;
+        a.mig_from = mig.from;
+        a.mig_to = mig.to;
+    }
+    const size_t lds_ids = attn_blk_slots(pool->block_size) * sizeof(int32_t) * (mig.dst ? 2 : 1);
     a.k_tab = pool->d_tab;
     a.q = static_cast<const uint8_t *>(q);
     a.tables = tables;
@@ -1056,8 +1075,7 @@ static int attn_enqueue(const llmig_pool *pool, const void *fn, const void *q, i
         a.item_base = first;
         a.items = m;
         void *args[] = {&a};
-        hipError_t e = hipLaunchKernel(fn, dim3(m * a.kv_heads, a.num_layers), dim3(kThreads), args,
-                                       attn_blk_slots(a.block_size) * sizeof(int32_t), st);
+        hipError_t e = hipLaunchKernel(fn, dim3(m * a.kv_heads, a.num_layers), dim3(kThreads), args, lds_ids, st);
         first += m;
         m = 0;
         return e;
@@ -1125,6 +1143,42 @@ int llmig_decode_attention(const llmig_pool *pool, int32_t dtype, const void *q,
         return LLMIG_EINVAL;
     return attn_enqueue(pool, fn, q, batch, q_heads, tables, table_stride, ctx_lens, scale,
                         static_cast<float *>(workspace), n_items, out, static_cast<hipStream_t>(stream));
+}
+
+int llmig_decode_attention_migrate(const llmig_pool *pool, int32_t dtype, const void *q, int32_t batch,
+                                   int32_t q_heads, const int32_t *tables, int32_t table_stride,
+                                   const int32_t *ctx_lens, float scale, void *workspace, int64_t workspace_bytes,
+                                   float *out, const llmig_pool *dst, int32_t seq, const int32_t *dst_ids,
+                                   int64_t from_block, int64_t to_block, void *stream)
+{
+    if (!dst || !pool || !ctx_lens || seq < 0 || seq >= batch || from_block < 0 || from_block > to_block)
+        return LLMIG_EINVAL;
+    if (from_block == to_block)     // nothing to carry: plain decode attention
+        return llmig_decode_attention(pool, dtype, q, batch, q_heads, tables, table_stride, ctx_lens, scale,
+                                      workspace, workspace_bytes, out, stream);
+    const void *fn = nullptr;
+    int64_t n_items = 0, need = 0;
+    int rc = attn_check(pool, dtype, q, batch, q_heads, tables, table_stride, ctx_lens, out, &fn, &n_items, &need,
+                        true);
+    if (rc != LLMIG_OK)
+        return rc;
+    if ((reinterpret_cast<uintptr_t>(workspace) & 15u) || !workspace || workspace_bytes < need)
+        return LLMIG_EINVAL;
+    // the destination: a second NHD pool of the same geometry on this device,
+    // apart from the source; the stage's blocks are whole blocks of the
+    // sequence's current length
+    if (dst == pool || !on_current_device(dst) || !same_geometry(pool, dst) || !same_layouts(pool, dst) ||
+        pools_overlap(pool, dst) || !dst_ids || (reinterpret_cast<uintptr_t>(dst_ids) & 3u) ||
+        to_block * pool->block_size > ctx_lens[seq])
+        return LLMIG_EINVAL;
+    AttnMigration mig;
+    mig.dst = dst;
+    mig.seq = seq;
+    mig.ids = dst_ids;
+    mig.from = static_cast<int32_t>(from_block);
+    mig.to = static_cast<int32_t>(to_block);
+    return attn_enqueue(pool, fn, q, batch, q_heads, tables, table_stride, ctx_lens, scale,
+                        static_cast<float *>(workspace), n_items, out, static_cast<hipStream_t>(stream), mig);
 }
 
 int llmig_decode_attention_noalloc(const llmig_pool *pool, int32_t dtype, const void *q, int32_t batch,

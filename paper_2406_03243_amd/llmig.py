@@ -106,6 +106,10 @@ _lib.llmig_decode_attention_workspace.restype = ctypes.c_int
 _lib.llmig_decode_attention.argtypes = [_vp, ctypes.c_int32, _vp, ctypes.c_int32, ctypes.c_int32, _vp,
                                         ctypes.c_int32, _vp, ctypes.c_float, _vp, ctypes.c_int64, _vp, _vp]
 _lib.llmig_decode_attention.restype = ctypes.c_int
+_lib.llmig_decode_attention_migrate.argtypes = [_vp, ctypes.c_int32, _vp, ctypes.c_int32, ctypes.c_int32, _vp,
+                                                ctypes.c_int32, _vp, ctypes.c_float, _vp, ctypes.c_int64, _vp,
+                                                _vp, ctypes.c_int32, _vp, ctypes.c_int64, ctypes.c_int64, _vp]
+_lib.llmig_decode_attention_migrate.restype = ctypes.c_int
 _lib.llmig_decode_attention_noalloc.argtypes = [_vp, ctypes.c_int32, _vp, ctypes.c_int32, ctypes.c_int32, _vp,
                                                 ctypes.c_int32, _vp, ctypes.c_float, _vp, _vp]
 _lib.llmig_decode_attention_noalloc.restype = ctypes.c_int
@@ -451,6 +455,28 @@ def llmig_decode_attention(pool: Pool, q: torch.Tensor, tables: torch.Tensor, ct
                                        workspace.numel() * workspace.element_size(), out.data_ptr(),
                                        _stream(stream)), "llmig_decode_attention")
     _used_on(stream, q, tables, workspace, out)
+
+
+def llmig_decode_attention_migrate(pool: Pool, q: torch.Tensor, tables: torch.Tensor, ctx_lens, scale: float,
+                                   workspace: torch.Tensor, out: torch.Tensor, dst: Pool, seq: int,
+                                   dst_ids: torch.Tensor, from_block: int, stream=None) -> None:
+    """llmig_decode_attention that also carries a migration stage: logical
+    blocks [from_block, from_block + len(dst_ids)) of sequence ``seq`` are
+    written into ``dst`` blocks ``dst_ids`` (a CUDA int32 tensor) as the
+    attention reads them."""
+    c = _attention_args(pool, q, tables, ctx_lens, out)
+    if not workspace.is_cuda or not workspace.is_contiguous():
+        raise ValueError("workspace must be a contiguous CUDA tensor")
+    if dst_ids.dtype != torch.int32 or not dst_ids.is_cuda or not dst_ids.is_contiguous() or dst_ids.dim() != 1:
+        raise ValueError("dst_ids must be a contiguous CUDA int32 vector")
+    _check(_lib.llmig_decode_attention_migrate(pool.handle, 1 if q.dtype == torch.bfloat16 else 0, q.data_ptr(),
+                                               q.shape[1], q.shape[2], tables.data_ptr(), tables.shape[1],
+                                               c.ctypes.data, float(scale), workspace.data_ptr(),
+                                               workspace.numel() * workspace.element_size(), out.data_ptr(),
+                                               dst.handle, int(seq), dst_ids.data_ptr(), int(from_block),
+                                               int(from_block) + dst_ids.numel(), _stream(stream)),
+           "llmig_decode_attention_migrate")
+    _used_on(stream, q, tables, workspace, out, dst_ids)
 
 
 def llmig_stream_read(region: torch.Tensor, passes: int, workgroups: int, out: torch.Tensor, stream=None) -> None:

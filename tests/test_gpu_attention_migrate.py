@@ -1,0 +1,185 @@
+"""GPU parity of llmig_decode_attention_migrate: a decode-attention pass
+that also carries a migration stage of one of its sequences (Llumnix §4.2
+stage copy, as a side effect of decode's reads of the same KV).
+
+Every case checks, through the C ABI, against the oracle:
+  * the attention output, to the error bound of tests/attn_cases.py, and
+    that it is the output of the plain llmig_decode_attention call;
+  * the destination pool, byte for byte over every block: the stage's
+    blocks hold what the oracle's tile copy of the same pairs writes and
+    every other block keeps its bytes;
+  * the source pool, unchanged.
+Cases cover head dims 64 and 128, block sizes 1-32, grouped and ungrouped
+heads, stages that start inside a partition and end inside another,
+sequences of several 2048-token partitions, a call split over two launches
+with the migrating sequence in both, and seeded random shapes."""
+import sys
+
+import numpy as np
+import pytest
+import torch
+
+import attn_cases as ac
+from oracle import HostPool
+from paper_2406_03243_amd import harness
+from paper_2406_03243_amd import workloads as wl
+
+pytestmark = pytest.mark.gpu
+
+if torch.cuda.is_available():
+    from paper_2406_03243_amd.llmig import (LlmigError, Pool, decode_workspace_bytes, llmig_decode_attention,
+                                            llmig_decode_attention_migrate)
+
+
+def say(*a):
+    print("[case]", *a, flush=True)
+    sys.stdout.flush()
+
+
+def to_device(shape: wl.PoolShape, host: HostPool):
+    k, v = harness.alloc_layers(shape)
+    for t, a in zip(k + v, host.k + host.v):
+        harness.tile_view(t).copy_(torch.from_numpy(a))
+    return Pool(k, v)
+
+
+def host_image(pool) -> HostPool:
+    return HostPool(harness.snapshot(pool.k), harness.snapshot(pool.v), pool.block_size, pool.slot_bytes)
+
+
+def dst_host(shape: wl.PoolShape, seed: int) -> HostPool:
+    tile = shape.block_size * shape.kv_heads * shape.head_dim * 2
+    draw = [wl.values16(seed, wl.DST_VALUES, shape.num_blocks * tile // 2, shape.dtype, sub=i).view(np.uint8)
+            .reshape(shape.num_blocks, tile) for i in range(2 * shape.num_layers)]
+    return HostPool(draw[:shape.num_layers], draw[shape.num_layers:], shape.block_size,
+                    shape.kv_heads * shape.head_dim * 2)
+
+
+def same_pool(got: HostPool, want: HostPool, what: str):
+    for l in range(want.num_layers):
+        for kv, (g, w) in enumerate(((got.k[l], want.k[l]), (got.v[l], want.v[l]))):
+            if not np.array_equal(g, w):
+                bad = np.argwhere((g != w).any(axis=1))[:, 0]
+                raise AssertionError(f"{what}: layer {l} {'KV'[kv]} blocks {bad[:8].tolist()} differ")
+
+
+def run_case(case, seq, from_block, to_block, seed, extra_dst_blocks=7):
+    num_layers, num_blocks, bs, kv_heads, head_dim, group, ctx, dtype, _ = case
+    host, qbits, tables, ctx, scale = ac.case_inputs(case, seed)
+    shape = wl.PoolShape(num_layers, num_blocks, bs, kv_heads, head_dim, dtype)
+    dshape = wl.PoolShape(num_layers, num_blocks + extra_dst_blocks, bs, kv_heads, head_dim, dtype)
+    hd = dst_host(dshape, seed)
+    src, dst = to_device(shape, host), to_device(dshape, hd)
+    g = wl.stream(seed, wl.EXTRA, 7)
+    ids = g.permutation(dshape.num_blocks)[:to_block - from_block].astype(np.int32)
+    dst_ids = torch.from_numpy(ids).cuda()
+    tdt = harness.TORCH_DTYPE[dtype]
+    q = torch.from_numpy(qbits.view(np.int16)).view(tdt).cuda()
+    tab = torch.from_numpy(tables).cuda()
+    out = torch.full(q.shape, float("nan"), dtype=torch.float32, device="cuda")
+    plain = torch.full(q.shape, float("nan"), dtype=torch.float32, device="cuda")
+    ws = torch.empty(max(16, decode_workspace_bytes(ctx, num_layers, q.shape[2], head_dim)), dtype=torch.uint8,
+                     device="cuda")
+    llmig_decode_attention_migrate(src, q, tab, ctx, scale, ws, out, dst, seq, dst_ids, from_block)
+    torch.cuda.synchronize()
+    llmig_decode_attention(src, q, tab, ctx, scale, ws, plain)
+    torch.cuda.synchronize()
+    orc = ac.default_oracle()
+    want = orc.decode_attention(host, kv_heads, head_dim, dtype, qbits, tables, ctx, scale)
+    tol = ac.tolerance(orc, host, kv_heads, head_dim, dtype, qbits, tables, ctx, scale)
+    got = out.cpu().numpy().astype(np.float64)
+    ratio = ac.excess(got, want, tol)
+    identical = torch.equal(out, plain)
+    say(f"max error / bound {ratio.max():.3g}; output identical to the plain call: {identical}")
+    assert not (~(ratio <= 1.0)).any(), f"bound ratio {np.nanmax(ratio):.3g}"
+    assert identical, "the carried stage changed the attention output"
+    orc.copy(host, hd, tables[seq, from_block:to_block], ids)
+    same_pool(host_image(dst), hd, "destination")
+    same_pool(host_image(src), host, "source")
+
+
+# (attention case, migrating sequence, first block, end block)
+CASES = [
+    (ac.CASES[0], 2, 0, 37),          # 600 tokens: all 37 full blocks, D 128, 8 heads a group
+    (ac.CASES[1], 0, 5, 32),          # starts inside the partition, D 64
+    (ac.CASES[2], 0, 0, 256),         # two partitions of 2048
+    (ac.CASES[2], 0, 100, 200),       # a range across the partition boundary
+    (ac.CASES[3], 1, 3, 11),          # 8-token blocks, 4 sequences
+    (ac.CASES[5], 1, 100, 7500),      # 133 items, two launches: sequence 1 spans both
+    (ac.CASES[7], 2, 0, 15),          # 4-token blocks
+    (ac.CASES[9], 1, 0, 625),         # 32-token blocks, ten partitions
+    (ac.CASES[6], 0, 42, 43),         # the last whole block of 700 tokens, 16 query heads on one KV head
+]
+
+
+def case_id(c):
+    return f"{ac.case_id(c[0])}_seq{c[1]}_blocks{c[2]}-{c[3]}"
+
+
+@pytest.mark.parametrize("c", CASES, ids=case_id)
+def test_attention_carries_stage(c):
+    case, seq, lo, hi = c
+    say("attention + stage", case_id(c))
+    run_case(case, seq, lo, hi, ac.case_seed(case))
+
+
+@pytest.mark.parametrize("seed", range(12))
+def test_attention_carries_stage_random(seed):
+    """Seeded random shapes (block sizes 1-32, head dims 64/128, groups,
+    batches, lengths) with a random sequence and block range."""
+    case = ac.random_case(40_000 + seed)
+    ctx = case[6]
+    g = wl.stream(40_000 + seed, wl.LENGTHS, 1)
+    full = [n // case[2] for n in ctx]
+    seq = int(np.argmax(full)) if g.random() < 0.5 else int(g.integers(0, len(ctx)))
+    lo = int(g.integers(0, full[seq] + 1))
+    hi = int(g.integers(lo, full[seq] + 1))
+    say("attention + stage random", seed, case, seq, lo, hi)
+    run_case(case, seq, lo, hi, 40_000 + seed)
+
+
+def test_attention_stage_rejects_bad_arguments():
+    """Argument errors are refused before anything is enqueued: the
+    destination pool keeps every byte."""
+    say("attention + stage errors")
+    shape = wl.PoolShape(1, 40, 16, 2, 64, "fp16")
+    host = dst_host(shape, 5)
+    src = to_device(shape, host)
+    hd = dst_host(wl.PoolShape(1, 40, 16, 2, 64, "fp16"), 6)
+    dst = to_device(shape, hd)
+    q = torch.zeros((1, 1, 4, 64), dtype=torch.float16, device="cuda")
+    tab = torch.arange(4, dtype=torch.int32, device="cuda").view(1, 4)
+    out = torch.zeros(q.shape, dtype=torch.float32, device="cuda")
+    ws = torch.zeros(1 << 20, dtype=torch.uint8, device="cuda")
+    ids = torch.arange(10, 14, dtype=torch.int32, device="cuda")
+    bad = [
+        dict(seq=1, from_block=0, dst_ids=ids[:2]),             # no sequence 1
+        dict(seq=-1, from_block=0, dst_ids=ids[:2]),
+        dict(seq=0, from_block=0, dst_ids=ids[:4]),             # 4 blocks of a 50-token sequence: 3 are whole
+        dict(seq=0, from_block=-1, dst_ids=ids[:2]),
+    ]
+    for kw in bad:
+        with pytest.raises(LlmigError):
+            llmig_decode_attention_migrate(src, q, tab, [50], 1.0, ws, out, dst, **kw)
+    # destination ids that are not 4-byte aligned, through the C ABI itself
+    from paper_2406_03243_amd import llmig as L
+    c = L._host_i32([50])
+    rc = L._lib.llmig_decode_attention_migrate(src.handle, 0, q.data_ptr(), 1, 4, tab.data_ptr(), 4, c.ctypes.data,
+                                               1.0, ws.data_ptr(), ws.numel(), out.data_ptr(), dst.handle, 0,
+                                               ids.data_ptr() + 2, 0, 2, None)
+    assert rc == -1, rc
+    with pytest.raises(LlmigError):                             # the source pool itself
+        llmig_decode_attention_migrate(src, q, tab, [50], 1.0, ws, out, src, 0, ids[:2], 0)
+    hk, hv = harness.alloc_layers(wl.PoolShape(1, 40, 16, 2, 128, "fp16"))
+    with pytest.raises(LlmigError):                             # other geometry
+        llmig_decode_attention_migrate(src, q, tab, [50], 1.0, ws, out, Pool(hk, hv), 0, ids[:2], 0)
+    torch.cuda.synchronize()
+    same_pool(host_image(dst), hd, "destination after refused calls")
+    # an empty stage is the plain call
+    llmig_decode_attention_migrate(src, q, tab, [50], 1.0, ws, out, dst, 0, ids[:0], 2)
+    plain = torch.zeros_like(out)
+    llmig_decode_attention(src, q, tab, [50], 1.0, ws, plain)
+    torch.cuda.synchronize()
+    assert torch.equal(out, plain)
+    same_pool(host_image(dst), hd, "destination after an empty stage")
+
