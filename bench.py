@@ -799,7 +799,78 @@ def decode_overhead(su, caps, step_ms, steps=14, reps=5):
             "step_us_during_migration_max": round(max(over), 1),
             "decode_slowdown_during_migration": round(statistics.mean(over) / t_alone - 1, 3),
             "downtime_us": round(statistics.median(r[2] for r in rows), 1)}
+    res["carried"] = carried_overhead(su, q, tables, ctx, scale, ws, out, at, mig, dec, steps, reps, t_alone)
     return res
+
+
+def carried_overhead(su, q, tables, ctx, scale, ws, out, at, mig, dec, steps, reps, t_alone, splits=(1, 4)):
+    """The same migration with its first stage carried by decode steps
+    (llmig_decode_attention_migrate): `split` consecutive steps of the
+    batch, the migrating request among their sequences, write its whole
+    blocks into the destination as their attention reads them; each step
+    adds the request's next token, and once the host has seen the last
+    carrying step complete, the final stage copies the rest beside the
+    steps that follow.  The decode time this costs is the carrying steps'
+    excess over a step alone, plus that of any step the final stage ran
+    beside."""
+    import torch
+
+    from paper_2406_03243_amd import migrate
+    from paper_2406_03243_amd.llmig import (llmig_decode_attention, llmig_decode_attention_migrate,
+                                            llmig_write_tokens)
+
+    src, dst, table, free = su.src, su.dst, su.tables[0], su.free
+    seq, initial = len(ctx) - 1, su.lengths[0]
+    append_pool = su.extra["append_pool"]
+    out_rows = {}
+    for split in splits:
+        rows = []
+        for r in range(reps):
+            m = migrate.Migration(src, dst, table, free, mig)
+            rec, _, md = m.plan(initial, final=False)
+            with torch.cuda.stream(at):
+                ids = torch.from_numpy(md).to("cuda")
+            bounds = [len(md) * k // split for k in range(split + 1)]
+            torch.cuda.synchronize()
+            evs = [torch.cuda.Event(enable_timing=True) for _ in range(steps + 1)]
+            evs[0].record(at)
+            for i in range(steps):
+                k = i - 2
+                if 0 <= k < split:
+                    llmig_decode_attention_migrate(src, q, tables, ctx, scale, ws, out, dst, seq,
+                                                   ids[bounds[k]:bounds[k + 1]], bounds[k], stream=at)
+                else:
+                    llmig_decode_attention(src, q, tables, ctx, scale, ws, out, stream=at)
+                evs[i + 1].record(at)
+            # each carrying step's token, written by decode
+            with torch.cuda.stream(dec):
+                data = append_pool[:, :, :split].contiguous()
+            dec.wait_event(evs[2])
+            llmig_write_tokens(src, table, initial, data, stream=dec)
+            evs[2 + split].synchronize()
+            dec.synchronize()
+            t0 = time.perf_counter()
+            m.finish(initial + split)
+            downtime = (m.finished_at - t0) * 1e6
+            m1 = torch.cuda.Event(enable_timing=True)
+            m1.record(mig)
+            torch.cuda.synchronize()
+            stop = evs[0].elapsed_time(m1)
+            st = [evs[i].elapsed_time(evs[i + 1]) * 1e3 for i in range(steps)]
+            over = [st[i] for i in range(2, steps) if i < 2 + split or evs[0].elapsed_time(evs[i]) < stop]
+            rows.append((st[2:2 + split], over, downtime))
+            m.abort()
+        carried = [x for c, _, _ in rows for x in c]
+        out_rows[f"split_{split}"] = {
+            "carrying_steps": split,
+            "stage_bytes_written": int(len(md) * su.shape.num_layers * 2 * src.tile_bytes),
+            "carrying_step_us_mean": round(statistics.mean(carried), 1),
+            "carrying_step_slowdown": round(statistics.mean(carried) / t_alone - 1, 3),
+            "extra_decode_us_per_migration": round(statistics.median(sum(x - t_alone for x in o)
+                                                                     for _, o, _ in rows), 1),
+            "overlapping_steps": round(statistics.mean(len(o) for _, o, _ in rows), 1),
+            "downtime_us": round(statistics.median(d for _, _, d in rows), 1)}
+    return out_rows
 
 
 if __name__ == "__main__":

@@ -55,6 +55,7 @@ struct AttnArgs {
     const uint64_t *dst_tab;
     const int32_t *mig_ids;
     int32_t mig_seq, mig_from, mig_to;
+    uint32_t dst_layer_bytes;   // bytes of one destination layer tensor (< 2^31)
 };
 
 struct AttnReduceArgs {
@@ -342,9 +343,15 @@ attn_partial_mfma(const AttnArgs a)
     // (slot of the token, head g, the chunk).  Rows of tokens past the
     // partition's end (loaded as copies of its last token) are skipped.
     auto store_group = [&](int32_t tg) {
-        uint8_t *const dk = reinterpret_cast<uint8_t *>(table_entry(a.dst_tab, layer));
-        uint8_t *const dv = reinterpret_cast<uint8_t *>(table_entry(a.dst_tab, a.num_layers + layer));
-        const uint64_t tile = static_cast<uint64_t>(a.block_size) * a.kv_heads * RB;
+        // raw buffer stores over the destination layer tensors, with the
+        // migration copy's cache policy (streaming, device scope); a whole
+        // 10.7 GB stage carried by one GQA decode step added 2.2-2.8 ms to
+        // the step with them, 2.8-2.9 ms with plain non-temporal stores
+        const __amdgpu_buffer_rsrc_t rk = tile_rsrc(
+            reinterpret_cast<const uint8_t *>(table_entry(a.dst_tab, layer)), a.dst_layer_bytes);
+        const __amdgpu_buffer_rsrc_t rv = tile_rsrc(
+            reinterpret_cast<const uint8_t *>(table_entry(a.dst_tab, a.num_layers + layer)), a.dst_layer_bytes);
+        const uint32_t tile = a.block_size * a.kv_heads * RB;
         int32_t dst_blk[KS];
         u32x4 r[KS];
 #pragma unroll
@@ -354,16 +361,16 @@ attn_partial_mfma(const AttnArgs a)
             r[j] = *reinterpret_cast<const u32x4 *>(kbuf + j * 1024 + lane * 16);
         }
         __builtin_amdgcn_s_waitcnt(kWaitLgkm0);
-        // where lane's row of instruction j starts in its destination tiles
+        // where lane's row of instruction j starts in the destination layer tensor
         auto row_off = [&](int j) {
             const int32_t t = tg + j * RPL + static_cast<int32_t>(lane / LPR);
-            return static_cast<uint64_t>(dst_blk[j]) * tile +
-                   (static_cast<uint64_t>(t % static_cast<int32_t>(a.block_size)) * a.kv_heads + g) * RB;
+            return static_cast<uint32_t>(dst_blk[j]) * tile +
+                   (static_cast<uint32_t>(t % static_cast<int32_t>(a.block_size)) * a.kv_heads + g) * RB;
         };
 #pragma unroll
         for (int j = 0; j < KS; ++j)
             if (dst_blk[j] >= 0)
-                store16(dk + row_off(j) + 16 * ((lane % LPR) ^ kswz(j * RPL + lane / LPR)), r[j]);
+                buffer_store16(rk, row_off(j) + 16 * ((lane % LPR) ^ kswz(j * RPL + lane / LPR)), r[j]);
 #pragma unroll
         for (int j = 0; j < KS; ++j)
             r[j] = *reinterpret_cast<const u32x4 *>(vbuf + j * 1024 + lane * 16);
@@ -371,7 +378,7 @@ attn_partial_mfma(const AttnArgs a)
 #pragma unroll
         for (int j = 0; j < KS; ++j)
             if (dst_blk[j] >= 0)
-                store16(dv + row_off(j) + 16 * (lane % LPR), r[j]);
+                buffer_store16(rv, row_off(j) + 16 * (lane % LPR), r[j]);
     };
     const int32_t tg0 = start + 16 * static_cast<int32_t>(wave);
     if (tg0 < end)
@@ -380,8 +387,10 @@ attn_partial_mfma(const AttnArgs a)
         // this group's rows have landed (the only loads in flight)
         __builtin_amdgcn_s_waitcnt(kWaitVm0);
         // a migrating launch stores the stage's rows first, while no operand
-        // fragments are live yet
-        if (MIG && mig)
+        // fragments are live yet; a group none of whose tokens lies in the
+        // stage's blocks skips it (a wavefront-uniform test)
+        if (MIG && mig && (tg + 15) / static_cast<int32_t>(a.block_size) >= a.mig_from &&
+            tg / static_cast<int32_t>(a.block_size) < a.mig_to)
             store_group(tg);
         // K fragments (A operand: token r16, dims 32*ks + 8*g4 .. +8)
         u32x4 kf[KS];

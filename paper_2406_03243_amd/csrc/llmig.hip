@@ -1054,6 +1054,7 @@ static int attn_enqueue(const llmig_pool *pool, const void *fn, const void *q, i
         a.mig_seq = mig.seq;
         a.mig_from = mig.from;
         a.mig_to = mig.to;
+        a.dst_layer_bytes = static_cast<uint32_t>(static_cast<uint64_t>(mig.dst->num_blocks) * mig.dst->tile_bytes);
     }
     const size_t lds_ids = attn_blk_slots(pool->block_size) * sizeof(int32_t) * (mig.dst ? 2 : 1);
     a.k_tab = pool->d_tab;
@@ -1169,7 +1170,8 @@ int llmig_decode_attention_migrate(const llmig_pool *pool, int32_t dtype, const 
     // sequence's current length
     if (dst == pool || !on_current_device(dst) || !same_geometry(pool, dst) || !same_layouts(pool, dst) ||
         pools_overlap(pool, dst) || !dst_ids || (reinterpret_cast<uintptr_t>(dst_ids) & 3u) ||
-        to_block * pool->block_size > ctx_lens[seq])
+        to_block * pool->block_size > ctx_lens[seq] ||
+        static_cast<uint64_t>(dst->num_blocks) * dst->tile_bytes > 0x7fffffffull)
         return LLMIG_EINVAL;
     AttnMigration mig;
     mig.dst = dst;

@@ -287,6 +287,50 @@ def run_timed(src: Pool, dst: Pool, src_table, initial_len: int, dst_free_list, 
     return m, downtime_us
 
 
+def run_carried(src: Pool, dst: Pool, src_table, initial_len: int, dst_free_list, decode_step, append_data,
+                attn_stream, mig_stream, dec_stream, split: int = 1):
+    """A migration whose first stage rides on decode steps (Llumnix §4.2's
+    stage 0, copied while the request keeps decoding): the coordinator
+    reserves and plans the stage (every whole block), and ``split`` decode
+    steps carry it, each writing its share of the blocks into ``dst`` as its
+    attention reads them (llmig_decode_attention_migrate).
+    ``decode_step(carry)`` enqueues one decode step on ``attn_stream``;
+    ``carry`` is (dst pool, device ids, first logical block) for the blocks
+    that step writes.  Each step produces one token of the request, which
+    decode writes on ``dec_stream`` from ``append_data`` ([L][K,V][n][slot
+    bytes], n >= split); it lands past the stage's blocks.  Once the host
+    has seen the steps and their writes complete, the request is drained
+    and a final stage on ``mig_stream`` copies the rest.  Returns
+    (migration, downtime_us, (start, end) events around the carrying steps
+    on ``attn_stream``)."""
+    m = Migration(src, dst, src_table, dst_free_list, mig_stream)
+    length = initial_len
+    rec, _, md = m.plan(length, final=False)
+    first = rec.from_tok // m.bs
+    with torch.cuda.stream(attn_stream):
+        ids = torch.from_numpy(md).to(attn_stream.device)
+    bounds = [len(md) * k // split for k in range(split + 1)]
+    t = (torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+    t[0].record(attn_stream)
+    for k in range(split):
+        decode_step((dst, ids[bounds[k]:bounds[k + 1]], first + bounds[k]))
+        with torch.cuda.stream(dec_stream):
+            data = append_data[:, :, k:k + 1].contiguous()
+        llmig_write_tokens(src, src_table, length, data, stream=dec_stream)
+        length += 1
+    t[1].record(attn_stream)
+    ev = _order_event()
+    ev.record(dec_stream)
+    t[1].synchronize()
+    ev.synchronize()
+    _spare_events.append(ev)
+    t0 = time.perf_counter()
+    m.finish(length)
+    downtime_us = (m.finished_at - t0) * 1e6
+    rec.gpu_us = t[0].elapsed_time(t[1]) * 1e3
+    return m, downtime_us, t
+
+
 def plan_batch(tables, lengths, dst_free_list, block_size: int):
     """Plan a batched migration of several requests as one stage each
     (request order, destination blocks taken from the head of the free list

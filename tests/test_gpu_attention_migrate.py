@@ -173,6 +173,10 @@ def test_attention_stage_rejects_bad_arguments():
     hk, hv = harness.alloc_layers(wl.PoolShape(1, 40, 16, 2, 128, "fp16"))
     with pytest.raises(LlmigError):                             # other geometry
         llmig_decode_attention_migrate(src, q, tab, [50], 1.0, ws, out, Pool(hk, hv), 0, ids[:2], 0)
+    big_k, big_v = harness.alloc_layers(wl.PoolShape(1, 1 << 19, 16, 2, 64, "fp16"))   # 2^31-byte layer tensors
+    with pytest.raises(LlmigError):                             # beyond the stores' 32-bit offsets
+        llmig_decode_attention_migrate(src, q, tab, [50], 1.0, ws, out, Pool(big_k, big_v), 0, ids[:2], 0)
+    del big_k, big_v
     torch.cuda.synchronize()
     same_pool(host_image(dst), hd, "destination after refused calls")
     # an empty stage is the plain call
@@ -183,3 +187,66 @@ def test_attention_stage_rejects_bad_arguments():
     assert torch.equal(out, plain)
     same_pool(host_image(dst), hd, "destination after an empty stage")
 
+
+
+@pytest.mark.parametrize("split", [1, 3])
+def test_migration_carried_by_decode_steps(split):
+    """A whole migration whose first stage rides on `split` decode steps of a
+    batch the request belongs to (migrate.run_carried): each step writes its
+    share of the request's whole blocks into the destination and produces
+    one token of the request; the final stage then copies the rest.  The
+    recorded schedule, replayed by the oracle, gives the destination byte
+    for byte, and every token of the request reads the same in both pools."""
+    import oracle
+    from paper_2406_03243_amd import migrate
+    shape = wl.PoolShape(2, 600, 16, 4, 128, "bf16")
+    seed = 8080 + split
+    say("migration carried by decode steps", split, shape)
+    host = dst_host(shape, seed + 1)
+    src = to_device(shape, host)
+    hd = dst_host(shape, seed)
+    dst = to_device(shape, hd)
+    g = wl.stream(seed, wl.EXTRA, 3)
+    perm = g.permutation(shape.num_blocks).astype(np.int32)
+    table, others = perm[:80], perm[80:]
+    initial = 79 * 16 + 5                       # 79 whole blocks and 5 tokens of the 80th
+    n_other, per = 3, 120
+    stride = max(per, len(table))
+    tabs = np.zeros((n_other + 1, stride), np.int32)
+    for k in range(n_other):
+        tabs[k, :per] = others[k * per:(k + 1) * per]
+    tabs[n_other, :len(table)] = table
+    ctx = [per * 16 - 7 * k for k in range(n_other)] + [initial]
+    q_heads = 16
+    qbits = wl.values16(seed, wl.APPEND_VALUES, shape.num_layers * len(ctx) * q_heads * shape.head_dim, "bf16", sub=9)
+    q = torch.from_numpy(qbits.view(np.int16)).view(torch.bfloat16).reshape(shape.num_layers, len(ctx), q_heads,
+                                                                             shape.head_dim).cuda()
+    tab = torch.from_numpy(tabs).cuda()
+    out = torch.empty(q.shape, dtype=torch.float32, device="cuda")
+    ws = torch.empty(decode_workspace_bytes([c + split for c in ctx], shape.num_layers, q_heads, shape.head_dim),
+                     dtype=torch.uint8, device="cuda")
+    append = wl.values16(seed, wl.APPEND_VALUES, shape.num_layers * 2 * split * src.slot_bytes // 2, "bf16", sub=4)
+    append = append.view(np.uint8).reshape(shape.num_layers, 2, split, src.slot_bytes)
+    (attn, mig, dec), _ = harness.concurrent_streams(3)
+    lengths = list(ctx)
+
+    def step(carry):
+        pool, ids, first = carry
+        llmig_decode_attention_migrate(src, q, tab, lengths, 0.125, ws, out, pool, n_other, ids, first, stream=attn)
+        lengths[n_other] += 1                   # the request's context grows by the step's token
+
+    free = np.ascontiguousarray(g.permutation(shape.num_blocks).astype(np.int32))
+    m, downtime, _ = migrate.run_carried(src, dst, table, initial, free, step, torch.from_numpy(append).cuda(),
+                                         attn, mig, dec, split=split)
+    torch.cuda.synchronize()
+    assert [r.from_tok for r in m.stages] == [0, 79 * 16] and m.stages[0].to_tok == 79 * 16
+    assert m.stages[-1].final and m.stages[-1].to_tok == initial + split and downtime > 0
+    events = [("stage", initial, 0, 79 * 16), ("append", initial, np.ascontiguousarray(append)),
+              ("stage", initial + split, 79 * 16, initial + split)]
+    hs = host.copy()
+    dst_table, _ = oracle.default().migrate(hs, hd, table, free, events)
+    assert np.array_equal(dst_table, m.commit())
+    gs, gd = host_image(src), host_image(dst)
+    same_pool(gs, hs, "source (with the appended tokens)")
+    same_pool(gd, hd, "destination")
+    assert oracle.default().first_token_mismatch(gs, table, gd, dst_table, initial + split) == -1
