@@ -398,9 +398,13 @@ int llmig_decode_attention(const llmig_pool *pool, int32_t dtype, const void *q,
  * to_block - from_block ids, 4-byte aligned, valid until the work
  * completes; the caller guarantees they are in [0, dst's num_blocks) and
  * distinct (as for llmig_stage with map_on_device = 1), which the
- * coordinator's llmig_migration_next gives.  Only whole blocks:
- * to_block * block_size <= ctx_lens[seq].  from_block == to_block is
- * llmig_decode_attention.  Errors: those of llmig_decode_attention, and
+ * coordinator's llmig_migration_next gives.  The blocks must hold tokens
+ * of the sequence: to_block <= ceil(ctx_lens[seq] / block_size).  A stage
+ * that ends in the sequence's partly filled last block (the final stage,
+ * carried by the request's last decode step on the source, so that no copy
+ * is left for after it is drained) writes the rows of its ctx_lens[seq]
+ * tokens; the block's slots past them keep the destination's bytes (they
+ * hold no token).  from_block == to_block is llmig_decode_attention.  Errors: those of llmig_decode_attention, and
  * LLMIG_EINVAL for a bad seq, block range, dst or dst_ids; nothing is
  * enqueued on an error. */
 int llmig_decode_attention_migrate(const llmig_pool *pool, int32_t dtype, const void *q, int32_t batch,

@@ -1166,11 +1166,11 @@ int llmig_decode_attention_migrate(const llmig_pool *pool, int32_t dtype, const 
     if ((reinterpret_cast<uintptr_t>(workspace) & 15u) || !workspace || workspace_bytes < need)
         return LLMIG_EINVAL;
     // the destination: a second NHD pool of the same geometry on this device,
-    // apart from the source; the stage's blocks are whole blocks of the
-    // sequence's current length
+    // apart from the source; the stage's blocks lie within the sequence's
+    // current length (its last block may be partly filled)
     if (dst == pool || !on_current_device(dst) || !same_geometry(pool, dst) || !same_layouts(pool, dst) ||
         pools_overlap(pool, dst) || !dst_ids || (reinterpret_cast<uintptr_t>(dst_ids) & 3u) ||
-        to_block * pool->block_size > ctx_lens[seq] ||
+        to_block > (static_cast<int64_t>(ctx_lens[seq]) + pool->block_size - 1) / pool->block_size ||
         static_cast<uint64_t>(dst->num_blocks) * dst->tile_bytes > 0x7fffffffull)
         return LLMIG_EINVAL;
     AttnMigration mig;

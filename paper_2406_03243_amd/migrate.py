@@ -288,7 +288,7 @@ def run_timed(src: Pool, dst: Pool, src_table, initial_len: int, dst_free_list, 
 
 
 def run_carried(src: Pool, dst: Pool, src_table, initial_len: int, dst_free_list, decode_step, append_data,
-                attn_stream, mig_stream, dec_stream, split: int = 1):
+                attn_stream, mig_stream, dec_stream, split: int = 1, carry_final: bool = False):
     """A migration whose first stage rides on decode steps (Llumnix §4.2's
     stage 0, copied while the request keeps decoding): the coordinator
     reserves and plans the stage (every whole block), and ``split`` decode
@@ -298,11 +298,16 @@ def run_carried(src: Pool, dst: Pool, src_table, initial_len: int, dst_free_list
     ``carry`` is (dst pool, device ids, first logical block) for the blocks
     that step writes.  Each step produces one token of the request, which
     decode writes on ``dec_stream`` from ``append_data`` ([L][K,V][n][slot
-    bytes], n >= split); it lands past the stage's blocks.  Once the host
-    has seen the steps and their writes complete, the request is drained
-    and a final stage on ``mig_stream`` copies the rest.  Returns
-    (migration, downtime_us, (start, end) events around the carrying steps
-    on ``attn_stream``)."""
+    bytes], n >= split); it lands past the stage's blocks.
+    Then the final stage.  By default the host waits for the steps and
+    their writes, the request is drained and a stage on ``mig_stream``
+    copies the rest (downtime: host wall time from its planning until the
+    host sees it complete).  With ``carry_final`` the request's last decode
+    step on the source carries the final stage itself (the rest, its partly
+    filled last block included, ordered after the last token's write), so
+    no copy is left once the request leaves the batch: downtime 0, and the
+    cost is that step's.  Returns (migration, downtime_us, (start, end)
+    events around the carrying steps on ``attn_stream``)."""
     m = Migration(src, dst, src_table, dst_free_list, mig_stream)
     length = initial_len
     rec, _, md = m.plan(length, final=False)
@@ -318,9 +323,24 @@ def run_carried(src: Pool, dst: Pool, src_table, initial_len: int, dst_free_list
             data = append_data[:, :, k:k + 1].contiguous()
         llmig_write_tokens(src, src_table, length, data, stream=dec_stream)
         length += 1
-    t[1].record(attn_stream)
     ev = _order_event()
     ev.record(dec_stream)
+    if carry_final:
+        rec_f, _, md_f = m.plan(length, final=True)
+        with torch.cuda.stream(attn_stream):
+            ids_f = torch.from_numpy(md_f).to(attn_stream.device)
+        attn_stream.wait_event(ev)              # the last token is written before the step reads it
+        t_f = torch.cuda.Event(enable_timing=True)
+        t_f.record(attn_stream)
+        decode_step((dst, ids_f, rec_f.from_tok // m.bs))
+        t[1].record(attn_stream)
+        t[1].synchronize()
+        _spare_events.append(ev)
+        rec.gpu_us = t[0].elapsed_time(t_f) * 1e3
+        rec_f.gpu_us = t_f.elapsed_time(t[1]) * 1e3
+        m.finished_at = time.perf_counter()
+        return m, 0.0, t
+    t[1].record(attn_stream)
     t[1].synchronize()
     ev.synchronize()
     _spare_events.append(ev)

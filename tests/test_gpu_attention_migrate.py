@@ -7,7 +7,9 @@ Every case checks, through the C ABI, against the oracle:
     that it is the output of the plain llmig_decode_attention call;
   * the destination pool, byte for byte over every block: the stage's
     blocks hold what the oracle's tile copy of the same pairs writes and
-    every other block keeps its bytes;
+    every other block keeps its bytes (a stage ending in the sequence's
+    partly filled last block writes that block's token rows only: its
+    slots past the length keep the destination's bytes);
   * the source pool, unchanged.
 Cases cover head dims 64 and 128, block sizes 1-32, grouped and ungrouped
 heads, stages that start inside a partition and end inside another,
@@ -63,6 +65,18 @@ def same_pool(got: HostPool, want: HostPool, what: str):
                 raise AssertionError(f"{what}: layer {l} {'KV'[kv]} blocks {bad[:8].tolist()} differ")
 
 
+def keep_tail(want: HostPool, before: HostPool, ids, to_block: int, length: int, bs: int):
+    """In the expected destination, give back the pre-stage bytes of the
+    slots past `length` in the stage's last block when that block is the
+    sequence's partly filled last one (no token lives there)."""
+    filled = length - (to_block - 1) * bs
+    if len(ids) == 0 or filled >= bs:
+        return
+    d, lo = int(ids[-1]), filled * want.slot_bytes
+    for a, b in zip(want.k + want.v, before.k + before.v):
+        a[d, lo:] = b[d, lo:]
+
+
 def run_case(case, seq, from_block, to_block, seed, extra_dst_blocks=7):
     num_layers, num_blocks, bs, kv_heads, head_dim, group, ctx, dtype, _ = case
     host, qbits, tables, ctx, scale = ac.case_inputs(case, seed)
@@ -93,7 +107,9 @@ def run_case(case, seq, from_block, to_block, seed, extra_dst_blocks=7):
     say(f"max error / bound {ratio.max():.3g}; output identical to the plain call: {identical}")
     assert not (~(ratio <= 1.0)).any(), f"bound ratio {np.nanmax(ratio):.3g}"
     assert identical, "the carried stage changed the attention output"
+    before = hd.copy()
     orc.copy(host, hd, tables[seq, from_block:to_block], ids)
+    keep_tail(hd, before, ids, to_block, ctx[seq], bs)
     same_pool(host_image(dst), hd, "destination")
     same_pool(host_image(src), host, "source")
 
@@ -109,6 +125,10 @@ CASES = [
     (ac.CASES[7], 2, 0, 15),          # 4-token blocks
     (ac.CASES[9], 1, 0, 625),         # 32-token blocks, ten partitions
     (ac.CASES[6], 0, 42, 43),         # the last whole block of 700 tokens, 16 query heads on one KV head
+    (ac.CASES[0], 2, 30, 38),         # ends in the partly filled last block (600 tokens: 8 in block 37)
+    (ac.CASES[3], 1, 0, 12),          # 95 tokens in 8-token blocks: the whole request, last block 7/8 full
+    (ac.CASES[7], 2, 10, 16),         # 62 tokens in 4-token blocks: the last block half full
+    (ac.CASES[5], 2, 1000, 1250),     # 20000 tokens, a sequence spanning both launches, last block full
 ]
 
 
@@ -130,7 +150,7 @@ def test_attention_carries_stage_random(seed):
     case = ac.random_case(40_000 + seed)
     ctx = case[6]
     g = wl.stream(40_000 + seed, wl.LENGTHS, 1)
-    full = [n // case[2] for n in ctx]
+    full = [-(-n // case[2]) for n in ctx]       # blocks holding tokens, the last one perhaps partly
     seq = int(np.argmax(full)) if g.random() < 0.5 else int(g.integers(0, len(ctx)))
     lo = int(g.integers(0, full[seq] + 1))
     hi = int(g.integers(lo, full[seq] + 1))
@@ -151,11 +171,11 @@ def test_attention_stage_rejects_bad_arguments():
     tab = torch.arange(4, dtype=torch.int32, device="cuda").view(1, 4)
     out = torch.zeros(q.shape, dtype=torch.float32, device="cuda")
     ws = torch.zeros(1 << 20, dtype=torch.uint8, device="cuda")
-    ids = torch.arange(10, 14, dtype=torch.int32, device="cuda")
+    ids = torch.arange(10, 15, dtype=torch.int32, device="cuda")
     bad = [
         dict(seq=1, from_block=0, dst_ids=ids[:2]),             # no sequence 1
         dict(seq=-1, from_block=0, dst_ids=ids[:2]),
-        dict(seq=0, from_block=0, dst_ids=ids[:4]),             # 4 blocks of a 50-token sequence: 3 are whole
+        dict(seq=0, from_block=0, dst_ids=ids[:5]),             # 5 blocks: a 50-token sequence holds 4
         dict(seq=0, from_block=-1, dst_ids=ids[:2]),
     ]
     for kw in bad:
@@ -189,19 +209,22 @@ def test_attention_stage_rejects_bad_arguments():
 
 
 
-@pytest.mark.parametrize("split", [1, 3])
-def test_migration_carried_by_decode_steps(split):
+@pytest.mark.parametrize("split,carry_final", [(1, False), (3, False), (1, True), (2, True)])
+def test_migration_carried_by_decode_steps(split, carry_final):
     """A whole migration whose first stage rides on `split` decode steps of a
     batch the request belongs to (migrate.run_carried): each step writes its
     share of the request's whole blocks into the destination and produces
-    one token of the request; the final stage then copies the rest.  The
-    recorded schedule, replayed by the oracle, gives the destination byte
-    for byte, and every token of the request reads the same in both pools."""
+    one token of the request; the final stage then copies the rest, as a
+    stage of its own after the drain or, with carry_final, carried by the
+    request's last decode step.  The recorded schedule, replayed by the
+    oracle, gives the destination byte for byte (a carried final stage
+    leaves the slots past the length in the last block as they were), and
+    every token of the request reads the same in both pools."""
     import oracle
     from paper_2406_03243_amd import migrate
     shape = wl.PoolShape(2, 600, 16, 4, 128, "bf16")
     seed = 8080 + split
-    say("migration carried by decode steps", split, shape)
+    say("migration carried by decode steps", split, carry_final, shape)
     host = dst_host(shape, seed + 1)
     src = to_device(shape, host)
     hd = dst_host(shape, seed)
@@ -237,15 +260,18 @@ def test_migration_carried_by_decode_steps(split):
 
     free = np.ascontiguousarray(g.permutation(shape.num_blocks).astype(np.int32))
     m, downtime, _ = migrate.run_carried(src, dst, table, initial, free, step, torch.from_numpy(append).cuda(),
-                                         attn, mig, dec, split=split)
+                                         attn, mig, dec, split=split, carry_final=carry_final)
     torch.cuda.synchronize()
     assert [r.from_tok for r in m.stages] == [0, 79 * 16] and m.stages[0].to_tok == 79 * 16
-    assert m.stages[-1].final and m.stages[-1].to_tok == initial + split and downtime > 0
+    assert m.stages[-1].final and m.stages[-1].to_tok == initial + split
+    assert downtime == 0.0 if carry_final else downtime > 0
     events = [("stage", initial, 0, 79 * 16), ("append", initial, np.ascontiguousarray(append)),
               ("stage", initial + split, 79 * 16, initial + split)]
-    hs = host.copy()
+    hs, before = host.copy(), hd.copy()
     dst_table, _ = oracle.default().migrate(hs, hd, table, free, events)
     assert np.array_equal(dst_table, m.commit())
+    if carry_final:
+        keep_tail(hd, before, dst_table, len(dst_table), initial + split, 16)
     gs, gd = host_image(src), host_image(dst)
     same_pool(gs, hs, "source (with the appended tokens)")
     same_pool(gd, hd, "destination")
