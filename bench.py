@@ -870,7 +870,73 @@ def carried_overhead(su, q, tables, ctx, scale, ws, out, at, mig, dec, steps, re
                                                                      for _, o, _ in rows), 1),
             "overlapping_steps": round(statistics.mean(len(o) for _, o, _ in rows), 1),
             "downtime_us": round(statistics.median(d for _, _, d in rows), 1)}
+    out_rows["split_1_final_carried"] = carried_final_overhead(su, q, tables, ctx, scale, out, at, dec, steps, reps,
+                                                               t_alone)
     return out_rows
+
+
+def carried_final_overhead(su, q, tables, ctx, scale, out, at, dec, steps, reps, t_alone):
+    """Both stages carried: step 2 of the batch carries stage 0 (every
+    whole block of the migrating request) and produces the request's next
+    token, which decode writes into its partly filled last block; step 3,
+    the request's last on the source, reads that token too and carries the
+    final stage (that block).  Once step 3 is over the destination holds the
+    whole request, so nothing is copied after it leaves the batch: no
+    downtime beyond the step.  The decode time this costs is the two
+    carrying steps' excess over a step alone."""
+    import torch
+
+    from paper_2406_03243_amd import migrate
+    from paper_2406_03243_amd.llmig import (decode_workspace_bytes, llmig_decode_attention,
+                                            llmig_decode_attention_migrate, llmig_write_tokens)
+
+    src, dst, table, free = su.src, su.dst, su.tables[0], su.free
+    seq, initial, bs = len(ctx) - 1, su.lengths[0], su.shape.block_size
+    ctx1 = list(ctx)
+    ctx1[seq] = initial + 1                       # the request after step 2's token
+    ws1 = torch.empty(decode_workspace_bytes(ctx1, su.shape.num_layers, q.shape[2], su.shape.head_dim),
+                      dtype=torch.uint8, device="cuda")
+    with torch.cuda.stream(dec):
+        data = su.extra["append_pool"][:, :, :1].contiguous()
+    rows = []
+    for r in range(reps):
+        m = migrate.Migration(src, dst, table, free, at)       # plans only: the steps carry the copies
+        rec0, _, md0 = m.plan(initial, final=False)
+        rec1, _, md1 = m.plan(initial + 1, final=True)
+        with torch.cuda.stream(at):
+            ids0 = torch.from_numpy(md0).to("cuda")
+            ids1 = torch.from_numpy(md1).to("cuda")
+        torch.cuda.synchronize()
+        evs = [torch.cuda.Event(enable_timing=True) for _ in range(steps + 1)]
+        written = torch.cuda.Event()
+        evs[0].record(at)
+        for i in range(steps):
+            if i == 2:
+                llmig_decode_attention_migrate(src, q, tables, ctx, scale, ws1, out, dst, seq, ids0,
+                                               rec0.from_tok // bs, stream=at)
+            elif i == 3:
+                at.wait_event(written)            # the token step 2 produced
+                llmig_decode_attention_migrate(src, q, tables, ctx1, scale, ws1, out, dst, seq, ids1,
+                                               rec1.from_tok // bs, stream=at)
+            else:
+                llmig_decode_attention(src, q, tables, ctx if i < 3 else ctx1, scale, ws1, out, stream=at)
+            evs[i + 1].record(at)
+            if i == 2:
+                dec.wait_event(evs[3])
+                llmig_write_tokens(src, table, initial, data, stream=dec)
+                written.record(dec)
+        torch.cuda.synchronize()
+        st = [evs[i].elapsed_time(evs[i + 1]) * 1e3 for i in range(steps)]
+        plain_after = statistics.median(st[5:])
+        rows.append((st[2], st[3], plain_after))
+        m.abort()
+    return {"carrying_steps": 2, "final_stage_blocks": len(md1),
+            "stage0_step_us_mean": round(statistics.mean(r[0] for r in rows), 1),
+            "final_step_us_mean": round(statistics.mean(r[1] for r in rows), 1),
+            "plain_step_us_after": round(statistics.mean(r[2] for r in rows), 1),
+            "extra_decode_us_per_migration": round(statistics.median(r[0] + r[1] - 2 * t_alone for r in rows), 1),
+            "downtime_us": 0.0,
+            "downtime_note": "the final stage completes with the request's last decode step on the source"}
 
 
 if __name__ == "__main__":
