@@ -346,39 +346,40 @@ attn_partial_mfma(const AttnArgs a)
         // raw buffer stores over the destination layer tensors, with the
         // migration copy's cache policy (streaming, device scope); a whole
         // 10.7 GB stage carried by one GQA decode step added 2.2-2.8 ms to
-        // the step with them, 2.8-2.9 ms with plain non-temporal stores
+        // the step with them, 2.8-2.9 ms with plain non-temporal stores.
+        // A row that is not the stage's gets an offset past the resource
+        // (layer tensors are under 2^31 bytes), so the range check drops
+        // its store and every store runs unpredicated.
+        constexpr uint32_t kDropped = 0x80000000u;
         const __amdgpu_buffer_rsrc_t rk = tile_rsrc(
             reinterpret_cast<const uint8_t *>(table_entry(a.dst_tab, layer)), a.dst_layer_bytes);
         const __amdgpu_buffer_rsrc_t rv = tile_rsrc(
             reinterpret_cast<const uint8_t *>(table_entry(a.dst_tab, a.num_layers + layer)), a.dst_layer_bytes);
         const uint32_t tile = a.block_size * a.kv_heads * RB;
-        int32_t dst_blk[KS];
+        const int32_t bs = static_cast<int32_t>(a.block_size);
+        const int32_t q = tg / bs, r0 = tg - q * bs;          // the group's first token: block, slot
+        uint32_t off[KS];
         u32x4 r[KS];
 #pragma unroll
         for (int j = 0; j < KS; ++j) {
-            const int32_t t = tg + j * RPL + static_cast<int32_t>(lane / LPR);
-            dst_blk[j] = t < end ? sh_dst[t / static_cast<int32_t>(a.block_size) - first_blk] : -1;
+            const int32_t tl = j * RPL + static_cast<int32_t>(lane / LPR);
+            const int32_t s = r0 + tl, bo = s / bs, slot = s - bo * bs;
+            const int32_t d = tg + tl < end ? sh_dst[q + bo - first_blk] : -1;
+            off[j] = d < 0 ? kDropped
+                           : static_cast<uint32_t>(d) * tile + (static_cast<uint32_t>(slot) * a.kv_heads + g) * RB;
             r[j] = *reinterpret_cast<const u32x4 *>(kbuf + j * 1024 + lane * 16);
         }
         __builtin_amdgcn_s_waitcnt(kWaitLgkm0);
-        // where lane's row of instruction j starts in the destination layer tensor
-        auto row_off = [&](int j) {
-            const int32_t t = tg + j * RPL + static_cast<int32_t>(lane / LPR);
-            return static_cast<uint32_t>(dst_blk[j]) * tile +
-                   (static_cast<uint32_t>(t % static_cast<int32_t>(a.block_size)) * a.kv_heads + g) * RB;
-        };
 #pragma unroll
         for (int j = 0; j < KS; ++j)
-            if (dst_blk[j] >= 0)
-                buffer_store16(rk, row_off(j) + 16 * ((lane % LPR) ^ kswz(j * RPL + lane / LPR)), r[j]);
+            buffer_store16(rk, off[j] + 16 * ((lane % LPR) ^ kswz(j * RPL + lane / LPR)), r[j]);
 #pragma unroll
         for (int j = 0; j < KS; ++j)
             r[j] = *reinterpret_cast<const u32x4 *>(vbuf + j * 1024 + lane * 16);
         __builtin_amdgcn_s_waitcnt(kWaitLgkm0);
 #pragma unroll
         for (int j = 0; j < KS; ++j)
-            if (dst_blk[j] >= 0)
-                buffer_store16(rv, row_off(j) + 16 * (lane % LPR), r[j]);
+            buffer_store16(rv, off[j] + 16 * (lane % LPR), r[j]);
     };
     const int32_t tg0 = start + 16 * static_cast<int32_t>(wave);
     if (tg0 < end)
