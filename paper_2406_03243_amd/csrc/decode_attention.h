@@ -219,7 +219,9 @@ __host__ __device__ inline uint32_t attn_blk_slots(uint32_t block_size)
 // place in the destination blocks.  Across the kv_heads workgroups of every
 // (layer, partition) that covers each whole tile, K and V, of those blocks,
 // so the destination receives exactly the bytes a pool-to-pool stage copy
-// would write, while HBM reads them once, for the attention.
+// would write, while HBM reads them once, for the attention (of the
+// sequence's partly filled last block, which only a final stage includes,
+// the rows of its tokens: the slots past them hold no token).
 template <int BF16, int D, int MIG>
 __global__ void __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(4, 8)))
 attn_partial_mfma(const AttnArgs a)
