@@ -129,6 +129,8 @@ CASES = [
     (ac.CASES[3], 1, 0, 12),          # 95 tokens in 8-token blocks: the whole request, last block 7/8 full
     (ac.CASES[7], 2, 10, 16),         # 62 tokens in 4-token blocks: the last block half full
     (ac.CASES[5], 2, 1000, 1250),     # 20000 tokens, a sequence spanning both launches, last block full
+    ((1, 2100, 1, 2, 64, 4, [2050, 7], "fp16", False), 0, 1000, 2050),   # 1-token blocks across a partition edge
+    ((2, 200, 32, 2, 128, 8, [1000, 70], "bf16", False), 0, 20, 32),     # 32-token blocks, last one 8/32 full
 ]
 
 
