@@ -398,8 +398,11 @@ int llmig_decode_attention(const llmig_pool *pool, int32_t dtype, const void *q,
  * to_block - from_block ids, 4-byte aligned, valid until the work
  * completes; the caller guarantees they are in [0, dst's num_blocks) and
  * distinct (as for llmig_stage with map_on_device = 1), which the
- * coordinator's llmig_migration_next gives.  The blocks must hold tokens
- * of the sequence: to_block <= ceil(ctx_lens[seq] / block_size).  A stage
+ * coordinator's llmig_migration_next gives.  The ids are not read on the
+ * host, so a bad one is not reported; a block whose id lies outside the
+ * pool is not written (no store can leave dst's layer tensors).  The
+ * blocks must hold tokens of the sequence:
+ * to_block <= ceil(ctx_lens[seq] / block_size).  A stage
  * that ends in the sequence's partly filled last block (the final stage,
  * carried by the request's last decode step on the source, so that no copy
  * is left for after it is drained) writes the rows of its ctx_lens[seq]

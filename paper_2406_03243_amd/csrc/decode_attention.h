@@ -56,6 +56,7 @@ struct AttnArgs {
     const int32_t *mig_ids;
     int32_t mig_seq, mig_from, mig_to;
     uint32_t dst_layer_bytes;   // bytes of one destination layer tensor (< 2^31)
+    int32_t dst_blocks;         // blocks of the destination pool
 };
 
 struct AttnReduceArgs {
@@ -288,7 +289,8 @@ attn_partial_mfma(const AttnArgs a)
     if (mig) {
         for (int32_t k = threadIdx.x; k < n_blk; k += kThreads) {
             const int32_t j = first_blk + k;
-            sh_dst[k] = j >= a.mig_from && j < a.mig_to ? a.mig_ids[j - a.mig_from] : -1;
+            const int32_t id = j >= a.mig_from && j < a.mig_to ? a.mig_ids[j - a.mig_from] : -1;
+            sh_dst[k] = id < a.dst_blocks ? id : -1;     // an id past the pool is not written
         }
     }
     __syncthreads();

@@ -1055,6 +1055,7 @@ static int attn_enqueue(const llmig_pool *pool, const void *fn, const void *q, i
         a.mig_from = mig.from;
         a.mig_to = mig.to;
         a.dst_layer_bytes = static_cast<uint32_t>(static_cast<uint64_t>(mig.dst->num_blocks) * mig.dst->tile_bytes);
+        a.dst_blocks = mig.dst->num_blocks;
     }
     const size_t lds_ids = attn_blk_slots(pool->block_size) * sizeof(int32_t) * (mig.dst ? 2 : 1);
     a.k_tab = pool->d_tab;

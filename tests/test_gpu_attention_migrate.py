@@ -160,6 +160,32 @@ def test_attention_carries_stage_random(seed):
     run_case(case, seq, lo, hi, 40_000 + seed)
 
 
+def test_attention_stage_skips_ids_outside_the_pool():
+    """Device destination ids are the caller's guarantee and are not read on
+    the host; an id past the destination pool or a negative one must still
+    not be written anywhere: the other blocks of the stage are copied and
+    every other destination block keeps its bytes."""
+    case = ac.CASES[1]
+    num_layers, num_blocks, bs, kv_heads, head_dim, group, _, dtype, _ = case
+    host, qbits, tables, ctx, scale = ac.case_inputs(case, ac.case_seed(case))
+    shape = wl.PoolShape(num_layers, num_blocks, bs, kv_heads, head_dim, dtype)
+    say("attention + stage, ids outside the pool", shape)
+    hd = dst_host(shape, 77)
+    src, dst = to_device(shape, host), to_device(shape, hd)
+    lo, hi = 2, 30
+    ids = wl.stream(77, wl.EXTRA, 7).permutation(num_blocks)[:hi - lo].astype(np.int32)
+    ids[1], ids[3] = num_blocks + 5, -3
+    q = torch.from_numpy(qbits.view(np.int16)).view(harness.TORCH_DTYPE[dtype]).cuda()
+    tab = torch.from_numpy(tables).cuda()
+    out = torch.empty(q.shape, dtype=torch.float32, device="cuda")
+    ws = torch.empty(decode_workspace_bytes(ctx, num_layers, q.shape[2], head_dim), dtype=torch.uint8, device="cuda")
+    llmig_decode_attention_migrate(src, q, tab, ctx, scale, ws, out, dst, 0, torch.from_numpy(ids).cuda(), lo)
+    torch.cuda.synchronize()
+    keep = np.array([k for k in range(hi - lo) if k not in (1, 3)])
+    ac.default_oracle().copy(host, hd, tables[0, lo:hi][keep], ids[keep])
+    same_pool(host_image(dst), hd, "destination")
+
+
 def test_attention_stage_rejects_bad_arguments():
     """Argument errors are refused before anything is enqueued: the
     destination pool keeps every byte."""
